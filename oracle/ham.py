@@ -190,18 +190,18 @@ class OracleHam:
         """Softmax attention: q [T][H][hd]; K, V [S][Hkv][hd]; row t sees slots < n_valid[t]."""
         s = self.s
         T, H, hd = q.shape
-        grp = H // s.n_kv_heads
+        kv_of = np.arange(H) // (H // s.n_kv_heads)     # q-head h reads kv-head h // (H / Hkv)
         out = np.zeros((T, H, hd))
         scale = 1.0 / math.sqrt(hd)
         for t in range(T):
             n = int(n_valid[t])
-            for h in range(H):
-                kv = h // grp
-                sc = K[:n, kv, :].astype(np.float64) @ q[t, h] * scale
-                sc = sc - sc.max()
-                a = np.exp(sc)
-                a /= a.sum()
-                out[t, h] = a @ V[:n, kv, :].astype(np.float64)
+            Kh = K[:n][:, kv_of, :].astype(np.float64)    # [n][H][hd]
+            Vh = V[:n][:, kv_of, :].astype(np.float64)
+            sc = np.einsum("hd,nhd->hn", q[t], Kh) * scale
+            sc = sc - sc.max(axis=1, keepdims=True)
+            a = np.exp(sc)
+            a /= a.sum(axis=1, keepdims=True)
+            out[t] = np.einsum("hn,nhd->hd", a, Vh)
         return out
 
     def forward_rows(self, layers: Sequence[_Layer], X: np.ndarray, pos: np.ndarray,

@@ -1,0 +1,128 @@
+// Device-side building blocks shared by every kernel of the library (gfx950).
+//
+// Storage types: `float` (fp32 models) and `bf16` (raw uint16 bit patterns of
+// bfloat16).  The matrix-core fragments below are the only place where the two
+// differ: one 16-byte load per lane per operand feeds either one
+// v_mfma_f32_16x16x32_bf16 (8 bf16 per lane) or four v_mfma_f32_16x16x4_f32
+// (4 fp32 per lane).  In both cases lane l of a wave holds operand row (l & 15)
+// and the k-slice owned by lane group g = l >> 4; the accumulator holds
+// D[4g + i][l & 15], i = 0..3.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ham {
+
+typedef uint16_t bf16;
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));  // one 16-byte lane fragment
+
+static constexpr int WAVE = 64;
+
+__device__ __forceinline__ float bf2f(bf16 u) { return __uint_as_float(((uint32_t)u) << 16); }
+
+// round to nearest even (values are finite by construction)
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f(T v);
+template <> __device__ __forceinline__ float to_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f<bf16>(bf16 v) { return bf2f(v); }
+
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f<bf16>(float v) { return f2bf(v); }
+
+// elements of T in one 16-byte lane fragment, and k covered by one wave fragment
+template <typename T> struct Frag;
+template <> struct Frag<bf16> {
+  static constexpr int EPL = 8;
+  static constexpr int KB = 32;
+  static __device__ __forceinline__ void mma(f4& acc, const u4& a, const u4& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  }
+};
+template <> struct Frag<float> {
+  static constexpr int EPL = 4;
+  static constexpr int KB = 16;
+  static __device__ __forceinline__ void mma(f4& acc, const u4& a, const u4& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ u4 ld16(const void* p) { return *reinterpret_cast<const u4*>(p); }
+// streamed once per step (weights, KV): non-temporal hint so they do not displace reused lines
+__device__ __forceinline__ u4 ld16_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u4*>(p));
+}
+__device__ __forceinline__ u4 zero16() { return u4{0u, 0u, 0u, 0u}; }
+
+// pack 8 floats (bf16) / 4 floats (fp32) into one lane fragment
+__device__ __forceinline__ u4 pack_frag_bf16(const float* v) {
+  u4 r;
+  r.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+  r.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  r.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+  r.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+  return r;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
+  return v;
+}
+
+// Block-wide sum for blockDim.x == 256 (4 waves); every thread gets the result.
+__device__ __forceinline__ float block_sum256(float v, float* sh4) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh4[w] = v;
+  __syncthreads();
+  return (sh4[0] + sh4[1]) + (sh4[2] + sh4[3]);
+}
+
+// Last-arriver handshake: every workgroup publishes its partial results, then
+// bumps `counter`; the one that sees `expected - 1` owns the final reduction and
+// resets the counter for the next launch.  No workgroup ever waits on another.
+// Every wave releases its own stores at agent scope first (the L2 of one XCD is
+// not coherent with the others for ordinary device memory); the owner acquires
+// before it reads what the others wrote.
+__device__ __forceinline__ bool last_arriver(int* counter, int expected, int* sh_flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    int last = (prev == expected - 1);
+    if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *sh_flag = last;
+  }
+  __syncthreads();
+  const bool last = *sh_flag != 0;
+  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  return last;
+}
+
+// any nonzero among n flags (n small); used to skip work no sequence needs
+__device__ __forceinline__ bool any_flag(const int* flags, int n) {
+  if (flags == nullptr) return true;
+  for (int i = 0; i < n; ++i)
+    if (flags[i]) return true;
+  return false;
+}
+
+}  // namespace ham

@@ -1,0 +1,592 @@
+// Host side of libham: configuration checks, buffer layouts, and the launch
+// sequences of prefill and of one macro-step.  Every arithmetic step runs in
+// the HIP kernels; this file only sequences them on the caller's stream.
+#include "../../include/ham.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "ham_internal.h"
+#include "kernels_misc.h"
+
+using namespace ham;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(call)                                                                       \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess) return fail(HAM_EHIP, "%s: %s", #call, hipGetErrorString(e_));    \
+  } while (0)
+
+size_t al(size_t x) { return (x + 255) & ~size_t(255); }
+int rup(int x, int m) { return (x + m - 1) / m * m; }
+
+uint64_t sm64(uint64_t s, uint64_t i) {
+  uint64_t z = s + (i + 1ull) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+constexpr int MAX_GEMM_SPLIT = 16;
+constexpr int MAX_ATTN_SPLIT = 64;
+constexpr int LOCAL_SLOTS = 64;
+
+struct Layout {
+  // dims
+  int L, M, d, H, Hk, hd, F, V, G, B, P, steps;
+  int QKV, HD, Vpad, S, max_pos, C, Tc, rows_dec, rows_max, Nmax, ctx_l[4];
+  size_t es;  // element size of the storage type
+  // weights
+  size_t E, Pe, Aqkv, Ao, Alin, Wlm, gf, gmf, cos_t, sin_t, w_bytes;
+  std::vector<size_t> Wqkv, Wo, Wgu, Wd, g1, g2;
+  // state
+  size_t Kc, VTc, kv_layer, seq, st_bytes;
+  // workspace
+  size_t x, xp, xn, qkv, q, ao, act, part, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
+      Kloc, VTloc, loc_layer, ws_bytes;
+};
+
+const char* check_cfg(const ham_config* c) {
+  if (!c) return "null config";
+  if (c->n_layers < 1 || c->d_model < 32 || c->n_heads < 1 || c->n_kv_heads < 1 || c->ffn_dim < 16 ||
+      c->vocab < 2 || c->micro_layers < 1)
+    return "dimensions must be positive (micro_layers >= 1)";
+  if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
+  if (c->n_heads % c->n_kv_heads != 0 || c->n_heads / c->n_kv_heads > 16) return "n_heads must be a multiple (<= 16x) of n_kv_heads";
+  if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32 || c->ffn_dim % 32) return "d_model, n_heads*head_dim and ffn_dim must be multiples of 32";
+  if (c->max_group < 1 || c->max_group > 4) return "max_group must be in 1..4";
+  if (c->stop_mode < 0 || c->stop_mode > 2) return "unknown stop_mode";
+  if (c->stop_mode == HAM_STOP_TOKEN && (c->stop_id < 0 || c->stop_id >= c->vocab)) return "stop_id out of range";
+  if (!(c->stop_conf >= 0.f && c->stop_conf <= 1.f)) return "stop_conf must be in [0, 1]";
+  if (c->dtype != HAM_F32 && c->dtype != HAM_BF16) return "dtype must be HAM_F32 or HAM_BF16";
+  if (c->max_batch < 1 || c->max_batch > 64) return "max_batch must be in 1..64";
+  if (c->max_prompt < 1 || c->max_steps < 0) return "max_prompt >= 1 and max_steps >= 0 required";
+  if ((long long)c->max_prompt + c->max_steps > (1 << 24)) return "capacity too large";
+  if (!(c->rope_theta > 1.f) || !(c->norm_eps > 0.f)) return "rope_theta > 1 and norm_eps > 0 required";
+  return nullptr;
+}
+
+Layout make_layout(const ham_config* c) {
+  Layout y;
+  y.L = c->n_layers; y.M = c->micro_layers; y.d = c->d_model; y.H = c->n_heads; y.Hk = c->n_kv_heads;
+  y.hd = c->head_dim; y.F = c->ffn_dim; y.V = c->vocab; y.G = c->max_group; y.B = c->max_batch;
+  y.P = c->max_prompt; y.steps = c->max_steps;
+  y.es = c->dtype == HAM_BF16 ? 2 : 4;
+  y.HD = y.H * y.hd;
+  y.QKV = (y.H + 2 * y.Hk) * y.hd;
+  y.Vpad = rup(y.V + 1, 32);
+  y.S = rup(y.P + y.steps, 64);
+  y.max_pos = y.P + y.G * (y.steps + 1) + 8;
+  y.C = std::min(4, y.L);
+  for (int i = 0; i < 4; ++i) y.ctx_l[i] = i < y.C ? (int)((long long)(i + 1) * y.L + y.C - 1) / y.C : -1;
+  y.Tc = std::min(y.P, 2048);
+  y.rows_dec = y.B * (y.C + 1);
+  y.rows_max = std::max(y.Tc, std::max(y.rows_dec, 5 * y.B));
+  y.Nmax = std::max(std::max(y.QKV, 2 * y.F), std::max(y.d, 3 * y.HD));
+  const size_t es = y.es;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o += al(bytes); return r; };
+  // weights
+  y.E = take((size_t)y.V * y.d * es);
+  y.Pe = take((size_t)4 * y.d * es);
+  y.Aqkv = take((size_t)3 * y.HD * y.d * es);
+  y.Ao = take((size_t)y.d * y.HD * es);
+  y.Alin = take((size_t)y.d * y.d * es);
+  y.Wlm = take((size_t)y.Vpad * y.d * es);
+  for (int j = 0; j < y.L + y.M; ++j) {
+    y.Wqkv.push_back(take((size_t)y.QKV * y.d * es));
+    y.Wo.push_back(take((size_t)y.d * y.HD * es));
+    y.Wgu.push_back(take((size_t)2 * y.F * y.d * es));
+    y.Wd.push_back(take((size_t)y.d * y.F * es));
+    y.g1.push_back(take((size_t)y.d * 4));
+    y.g2.push_back(take((size_t)y.d * 4));
+  }
+  y.gf = take((size_t)y.d * 4);
+  y.gmf = take((size_t)y.d * 4);
+  y.cos_t = take((size_t)y.max_pos * (y.hd / 2) * 4);
+  y.sin_t = take((size_t)y.max_pos * (y.hd / 2) * 4);
+  y.w_bytes = o;
+  // state: smashed KV cache (K slot-major, V d-major) and per-sequence counters
+  o = 0;
+  y.kv_layer = al((size_t)y.B * y.Hk * y.S * y.hd * es);
+  y.Kc = take(y.kv_layer * y.L);
+  y.VTc = take(y.kv_layer * y.L);
+  y.seq = take((size_t)y.B * 4 * 32);
+  y.st_bytes = o;
+  // workspace
+  o = 0;
+  const size_t R = y.rows_max;
+  y.x = take((size_t)y.rows_dec * y.d * 4);
+  y.xp = take((size_t)y.Tc * y.d * 4);
+  y.xn = take(R * std::max(y.d, y.HD) * es);
+  y.qkv = take(R * std::max(y.QKV, 3 * y.HD) * 4);
+  y.q = take(R * y.HD * es);
+  y.ao = take(R * y.HD * es);
+  y.act = take(R * y.F * es);
+  y.part = take((size_t)MAX_GEMM_SPLIT * 64 * y.Nmax * 4);
+  y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
+  y.actr = take((size_t)y.rows_dec * y.Hk * 4);
+  y.apart = take((size_t)y.rows_dec * y.Hk * MAX_ATTN_SPLIT * (y.H / y.Hk) * (y.hd + 2) * 4);
+  y.bval = take((size_t)(y.Vpad / 32) * 64 * 4);
+  y.bidx = take((size_t)(y.Vpad / 32) * 64 * 4);
+  y.stopb = take(64 * 4);
+  y.ctx = take((size_t)y.B * y.C * y.d * 4);
+  y.emb_in = take((size_t)5 * y.B * y.d * es);
+  y.emb_o = take((size_t)y.B * y.HD * es);
+  y.emb_y = take((size_t)y.B * y.d * es);
+  y.loc_layer = al((size_t)y.B * y.Hk * LOCAL_SLOTS * y.hd * es);
+  y.Kloc = take(y.loc_layer * y.M);
+  y.VTloc = take(y.loc_layer * y.M);
+  y.ws_bytes = o;
+  return y;
+}
+
+}  // namespace
+
+struct ham_model {
+  ham_config cfg;
+  Layout y;
+  char* w;
+  char* st;
+  char* ws;
+  hipStream_t s;
+  SeqPtrs sp;
+  int batch = 0, prompt_len = 0, steps_done = -1, has_teacher = 0;
+  float tau;
+  float* dbg = nullptr;
+  // typed views
+  template <typename P> P* W(size_t off) const { return (P*)(w + off); }
+  template <typename P> P* WS(size_t off) const { return (P*)(ws + off); }
+};
+
+namespace {
+
+SeqPtrs seq_ptrs(char* st, const Layout& y) {
+  int* base = (int*)(st + y.seq);
+  const int B = y.B;
+  SeqPtrs p;
+  int* q = base;
+  auto next = [&](int n) { int* r = q; q += (size_t)n * B; return r; };
+  p.kv_len = next(1); p.pos_last = next(1); p.cur_pos = next(1); p.cur_slot = next(1);
+  p.emitted = next(1); p.budget = next(1); p.done = next(1); p.groups = next(1);
+  p.hist = next(5); p.step_on = next(1); p.fused = next(1); p.active = next(1);
+  p.grp_n = next(1); p.grp_tok = next(4); p.forced = next(1); p.teacher = next(4); p.err = next(1);
+  return p;
+}
+
+int dtype_of(const ham_model* m) { return m->cfg.dtype; }
+
+// one transformer layer (base layer j < L, micro layer j >= L) over R rows
+int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefill, void* Kc, void* VTc,
+              long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, float* ctx_out,
+              int ldctx) {
+  const Layout& y = m->y;
+  const int dt = dtype_of(m);
+  hipStream_t s = m->s;
+  NormArgs na{};
+  na.x = x; na.ldx = y.d; na.row_stride = 1; na.row_off = 0; na.g = m->W<float>(y.g1[j]); na.d = y.d; na.R = R;
+  na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d; na.gate = gate; na.gate_n = gate_n;
+  launch_rmsnorm(dt, na, s);
+
+  GemmArgs ga{};
+  ga.part = m->WS<float>(y.part); ga.counters = m->WS<int>(y.gctr); ga.gate = gate; ga.gate_n = gate_n;
+  ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = R;
+  ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
+  if (launch_gemm(dt, EPI_F32, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "qkv gemm shape");
+
+  RopeArgs ra{};
+  ra.qkv = m->WS<float>(y.qkv); ra.ldqkv = y.QKV; ra.R = R; ra.q = m->WS<char>(y.q); ra.ldq = y.HD;
+  ra.K = Kc; ra.VT = VTc; ra.sb = sb; ra.sh = sh; ra.S = S; ra.H = y.H; ra.Hkv = y.Hk; ra.hd = y.hd;
+  ra.cos_t = m->W<float>(y.cos_t); ra.sin_t = m->W<float>(y.sin_t); ra.max_pos = y.max_pos; ra.rm = rm;
+  ra.gate = gate; ra.gate_n = gate_n;
+  launch_rope_append(dt, ra, s);
+
+  AttnArgs aa{};
+  aa.q = m->WS<char>(y.q); aa.ldq = y.HD; aa.K = Kc; aa.VT = VTc; aa.sb = sb; aa.sh = sh; aa.S = S;
+  aa.H = y.H; aa.Hkv = y.Hk; aa.hd = y.hd; aa.R = R; aa.nsplit = attn_split; aa.o = m->WS<char>(y.ao);
+  aa.ldo = y.HD; aa.part = m->WS<float>(y.apart); aa.counters = m->WS<int>(y.actr); aa.rm = rm;
+  aa.gate = gate; aa.gate_n = gate_n;
+  if ((prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s)) != 0)
+    return fail(HAM_EINVAL, "attention shape");
+
+  ga.W = m->W<char>(y.Wo[j]); ga.N = y.d; ga.K = y.HD; ga.X = m->WS<char>(y.ao); ga.ldx = y.HD;
+  ga.out = x; ga.ldo = y.d;
+  if (launch_gemm(dt, EPI_RESID, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "o-proj gemm shape");
+
+  na.g = m->W<float>(y.g2[j]);
+  launch_rmsnorm(dt, na, s);
+
+  ga.W = m->W<char>(y.Wgu[j]); ga.N = 2 * y.F; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+  ga.out = m->WS<char>(y.act); ga.ldo = y.F;
+  if (launch_gemm(dt, EPI_SWIGLU, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "gate/up gemm shape");
+
+  ga.W = m->W<char>(y.Wd[j]); ga.N = y.d; ga.K = y.F; ga.X = m->WS<char>(y.act); ga.ldx = y.F;
+  ga.out = x; ga.ldo = y.d; ga.ctx = ctx_out; ga.ldctx = ldctx;
+  if (launch_gemm(dt, EPI_RESID, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "down gemm shape");
+  return HAM_OK;
+}
+
+// final norm of one row per sequence + LM head argmax + stop head + stop test (decision k)
+int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, const float* g,
+                 int* out_tokens, int* out_lens) {
+  const Layout& y = m->y;
+  const int dt = dtype_of(m);
+  const int B = m->batch;
+  NormArgs na{};
+  na.x = x; na.ldx = y.d; na.row_stride = row_stride; na.row_off = row_off; na.g = g; na.d = y.d; na.R = B;
+  na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d;
+  na.hid = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + ((size_t)k * y.B) * y.d : nullptr; na.ldh = y.d;
+  na.gate = m->sp.active; na.gate_n = B;
+  launch_rmsnorm(dt, na, m->s);
+
+  GemmArgs ga{};
+  ga.W = m->W<char>(y.Wlm); ga.N = y.Vpad; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = B;
+  ga.counters = m->WS<int>(y.gctr); ga.gate = m->sp.active; ga.gate_n = B;
+  DecideArgs& d = ga.dec;
+  d.st = m->sp; d.B = B; d.k = k; d.mode = m->cfg.stop_mode; d.stop_id = m->cfg.stop_id; d.G = y.G; d.V = y.V;
+  d.tau = m->tau; d.out_tokens = out_tokens; d.out_lens = out_lens; d.has_teacher = m->has_teacher;
+  d.dbg_logits = m->dbg ? m->dbg + (size_t)k * y.B * y.V : nullptr;
+  d.dbg_stop = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + (size_t)4 * y.B * y.d + (size_t)k * y.B : nullptr;
+  d.stop_buf = m->WS<float>(y.stopb); d.best_val = m->WS<float>(y.bval); d.best_idx = m->WS<int>(y.bidx);
+  if (launch_gemm(dt, EPI_ARGMAX, ga, 1, m->s)) return fail(HAM_EINVAL, "lm head shape");
+  return HAM_OK;
+}
+
+// decision k = 0 from the base model, then the micro steps (all gated on device)
+int decode_tail(ham_model* m, int* out_tokens, int* out_lens) {
+  const Layout& y = m->y;
+  const int dt = dtype_of(m);
+  const int B = m->batch;
+  float* x = m->WS<float>(y.x);
+  int rc = run_decision(m, 0, x, 1, 0, m->W<float>(y.gf), out_tokens, out_lens);
+  if (rc) return rc;
+  const long long lsb = (long long)y.Hk * LOCAL_SLOTS * y.hd, lsh = (long long)LOCAL_SLOTS * y.hd;
+  for (int k = 1; k < y.G; ++k) {
+    MicroPrepArgs mp{};
+    mp.st = m->sp; mp.B = B; mp.C = y.C; mp.k = k; mp.d = y.d; mp.ctx = m->WS<float>(y.ctx);
+    mp.E = m->W<char>(y.E); mp.x = x;
+    launch_micro_prep(dt, mp, m->s);
+    RowMap rm{};
+    rm.mode = k == 1 ? ROWS_MICRO1 : ROWS_MICROK; rm.C = y.C; rm.k = k; rm.st = m->sp;
+    const int R = k == 1 ? B * (y.C + 1) : B;
+    for (int mj = 0; mj < y.M; ++mj) {
+      rc = run_layer(m, y.L + mj, R, rm, x, false, m->WS<char>(y.Kloc + mj * y.loc_layer),
+                     m->WS<char>(y.VTloc + mj * y.loc_layer), lsb, lsh, LOCAL_SLOTS, 1, m->sp.active, B,
+                     nullptr, 0);
+      if (rc) return rc;
+    }
+    rc = run_decision(m, k, x, k == 1 ? y.C + 1 : 1, k == 1 ? y.C : 0, m->W<float>(y.gmf), out_tokens,
+                      out_lens);
+    if (rc) return rc;
+  }
+  return HAM_OK;
+}
+
+int attn_splits(const ham_model* m, int R, int kv_max) {
+  const int kb = m->cfg.dtype == HAM_BF16 ? 32 : 16;
+  int want = (2048 + R * m->y.Hk - 1) / (R * m->y.Hk);
+  const int most = std::max(1, (kv_max + 2 * kb - 1) / (2 * kb));
+  return std::max(1, std::min(std::min(want, most), MAX_ATTN_SPLIT));
+}
+
+}  // namespace
+
+// ============================================================================ C ABI
+extern "C" {
+
+const char* ham_last_error(void) { return g_err.c_str(); }
+
+size_t ham_weights_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_layout(c).w_bytes; }
+size_t ham_state_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_layout(c).st_bytes; }
+size_t ham_workspace_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_layout(c).ws_bytes; }
+
+int ham_tensor_info(const ham_config* c, int32_t id, size_t* offset, int32_t* rows, int32_t* cols,
+                    int32_t* interleave) {
+  if (const char* e = check_cfg(c)) return fail(HAM_EINVAL, "%s", e);
+  if (!offset || !rows || !cols || !interleave) return fail(HAM_EINVAL, "null output pointer");
+  const Layout y = make_layout(c);
+  *interleave = 0;
+  const size_t es = y.es;
+  switch (id) {
+    case 0: *offset = y.E; *rows = y.V; *cols = y.d; return HAM_OK;
+    case 1: *offset = y.Pe; *rows = 4; *cols = y.d; return HAM_OK;
+    case 2: case 3: case 4:
+      *offset = y.Aqkv + (size_t)(id - 2) * y.HD * y.d * es; *rows = y.HD; *cols = y.d; return HAM_OK;
+    case 5: *offset = y.Ao; *rows = y.d; *cols = y.HD; return HAM_OK;
+    case 6: *offset = y.Alin; *rows = y.d; *cols = y.d; return HAM_OK;
+    case 7: *offset = y.Wlm; *rows = y.V; *cols = y.d; return HAM_OK;
+    case 8: *offset = y.Wlm + (size_t)y.V * y.d * es; *rows = 1; *cols = y.d; return HAM_OK;
+    default: break;
+  }
+  if (id < 16) return fail(HAM_EINVAL, "unknown tensor id %d", id);
+  const int j = (id - 16) / 8, t = (id - 16) % 8;
+  if (j >= y.L + y.M || t > 6) return fail(HAM_EINVAL, "unknown tensor id %d", id);
+  switch (t) {
+    case 0: *offset = y.Wqkv[j]; *rows = y.HD; *cols = y.d; break;
+    case 1: *offset = y.Wqkv[j] + (size_t)y.HD * y.d * es; *rows = y.Hk * y.hd; *cols = y.d; break;
+    case 2: *offset = y.Wqkv[j] + (size_t)(y.HD + y.Hk * y.hd) * y.d * es; *rows = y.Hk * y.hd; *cols = y.d; break;
+    case 3: *offset = y.Wo[j]; *rows = y.d; *cols = y.HD; break;
+    case 4: *offset = y.Wgu[j]; *rows = y.F; *cols = y.d; *interleave = 1; break;
+    case 5: *offset = y.Wgu[j]; *rows = y.F; *cols = y.d; *interleave = 2; break;
+    case 6: *offset = y.Wd[j]; *rows = y.d; *cols = y.F; break;
+  }
+  return HAM_OK;
+}
+
+int ham_init_weights(const ham_config* c, uint64_t seed, void* d_weights, size_t weights_bytes, void* d_state,
+                     size_t state_bytes, void* d_workspace, size_t workspace_bytes, void* hip_stream,
+                     ham_model** out) {
+  if (!out) return fail(HAM_EINVAL, "null output handle");
+  *out = nullptr;
+  if (const char* e = check_cfg(c)) return fail(HAM_EINVAL, "%s", e);
+  if (!d_weights || !d_state || !d_workspace) return fail(HAM_EINVAL, "null buffer");
+  const Layout y = make_layout(c);
+  if (weights_bytes < y.w_bytes || state_bytes < y.st_bytes || workspace_bytes < y.ws_bytes)
+    return fail(HAM_ENOMEM, "buffers too small (need %zu / %zu / %zu bytes)", y.w_bytes, y.st_bytes, y.ws_bytes);
+  if (((uintptr_t)d_weights | (uintptr_t)d_state | (uintptr_t)d_workspace) & 255)
+    return fail(HAM_EINVAL, "buffers must be 256-byte aligned");
+  ham_model* m = new ham_model();
+  m->cfg = *c;
+  m->y = y;
+  m->w = (char*)d_weights;
+  m->st = (char*)d_state;
+  m->ws = (char*)d_workspace;
+  m->s = (hipStream_t)hip_stream;
+  m->sp = seq_ptrs(m->st, y);
+  const double cf = c->stop_conf;
+  m->tau = cf <= 0.0 ? INFINITY : (cf >= 1.0 ? -INFINITY : (float)std::log((1.0 - cf) / cf));
+  const int dt = c->dtype;
+  hipStream_t s = m->s;
+  auto bad = [&](int rc) { delete m; return rc; };
+#define INIT_TRY(call)                                                                      \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess) return bad(fail(HAM_EHIP, "%s: %s", #call, hipGetErrorString(e_))); \
+  } while (0)
+  INIT_TRY(hipMemsetAsync(d_weights, 0, y.w_bytes, s));
+  INIT_TRY(hipMemsetAsync(d_state, 0, y.st_bytes, s));
+  INIT_TRY(hipMemsetAsync(d_workspace, 0, y.ws_bytes, s));
+  auto gen = [&](size_t off, int rows, int cols, long long row_off, int inter, int tid) {
+    GenArgs g{};
+    g.dst = m->w + off; g.rows = rows; g.cols = cols; g.row_off = row_off; g.interleave = inter;
+    g.key = sm64(seed, (uint64_t)tid);
+    launch_gen_normal(dt, g, s);
+  };
+  gen(y.E, y.V, y.d, 0, 0, 0);
+  gen(y.Pe, 4, y.d, 0, 0, 1);
+  for (int i = 0; i < 3; ++i) gen(y.Aqkv, y.HD, y.d, (long long)i * y.HD, 0, 2 + i);
+  gen(y.Ao, y.d, y.HD, 0, 0, 5);
+  gen(y.Alin, y.d, y.d, 0, 0, 6);
+  gen(y.Wlm, y.V, y.d, 0, 0, 7);
+  gen(y.Wlm, 1, y.d, y.V, 0, 8);
+  for (int j = 0; j < y.L + y.M; ++j) {
+    const int base = 16 + 8 * j;
+    gen(y.Wqkv[j], y.HD, y.d, 0, 0, base + 0);
+    gen(y.Wqkv[j], y.Hk * y.hd, y.d, y.HD, 0, base + 1);
+    gen(y.Wqkv[j], y.Hk * y.hd, y.d, y.HD + y.Hk * y.hd, 0, base + 2);
+    gen(y.Wo[j], y.d, y.HD, 0, 0, base + 3);
+    gen(y.Wgu[j], y.F, y.d, 0, 1, base + 4);
+    gen(y.Wgu[j], y.F, y.d, 0, 2, base + 5);
+    gen(y.Wd[j], y.d, y.F, 0, 0, base + 6);
+    launch_fill_f32(m->W<float>(y.g1[j]), y.d, 1.0f, s);
+    launch_fill_f32(m->W<float>(y.g2[j]), y.d, 1.0f, s);
+  }
+  launch_fill_f32(m->W<float>(y.gf), y.d, 1.0f, s);
+  launch_fill_f32(m->W<float>(y.gmf), y.d, 1.0f, s);
+  INIT_TRY(hipGetLastError());
+  // RoPE tables: angle p * theta^(-2i/hd) in float64, cos/sin rounded to fp32
+  const int half = y.hd / 2;
+  std::vector<float> ct((size_t)y.max_pos * half), stt((size_t)y.max_pos * half);
+  for (int i = 0; i < half; ++i) {
+    const double inv = std::pow((double)c->rope_theta, -2.0 * i / (double)y.hd);
+    for (int p = 0; p < y.max_pos; ++p) {
+      const double a = (double)p * inv;
+      ct[(size_t)p * half + i] = (float)std::cos(a);
+      stt[(size_t)p * half + i] = (float)std::sin(a);
+    }
+  }
+  INIT_TRY(hipMemcpyAsync(m->w + y.cos_t, ct.data(), ct.size() * 4, hipMemcpyHostToDevice, s));
+  INIT_TRY(hipMemcpyAsync(m->w + y.sin_t, stt.data(), stt.size() * 4, hipMemcpyHostToDevice, s));
+  INIT_TRY(hipStreamSynchronize(s));
+#undef INIT_TRY
+  *out = m;
+  return HAM_OK;
+}
+
+int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t prompt_len, const int32_t* h_max_new,
+                const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  const Layout& y = m->y;
+  if (batch < 1 || prompt_len < 1 || !d_prompt || !h_max_new || !d_out_tokens || !d_out_lens)
+    return fail(HAM_EINVAL, "bad prefill arguments");
+  if (batch > y.B || prompt_len > y.P)
+    return fail(HAM_ECAP, "batch %d / prompt %d exceed capacity %d / %d", batch, prompt_len, y.B, y.P);
+  if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
+  if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
+  for (int b = 0; b < batch; ++b)
+    if (h_max_new[b] < 0) return fail(HAM_EINVAL, "negative budget");
+  const int dt = dtype_of(m);
+  hipStream_t s = m->s;
+  m->batch = batch;
+  m->prompt_len = prompt_len;
+  m->steps_done = -1;
+  m->has_teacher = d_teacher != nullptr;
+  // budgets are read by kernels of earlier calls: let those finish, then copy synchronously
+  HIP_TRY(hipStreamSynchronize(s));
+  HIP_TRY(hipMemcpy(m->sp.budget, h_max_new, sizeof(int32_t) * batch, hipMemcpyHostToDevice));
+  PrefillArgs pa{};
+  pa.st = m->sp; pa.B = batch; pa.P = prompt_len; pa.G = y.G; pa.forced_in = d_forced_lens;
+  pa.teacher_in = d_teacher; pa.out_tokens = d_out_tokens; pa.out_lens = d_out_lens;
+  launch_prefill_begin(pa, s);
+  float* xp = m->WS<float>(y.xp);
+  float* x = m->WS<float>(y.x);
+  float* ctx = m->WS<float>(y.ctx);
+  const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
+  for (int b = 0; b < batch; ++b) {
+    for (int t0 = 0; t0 < prompt_len; t0 += y.Tc) {
+      const int R = std::min(y.Tc, prompt_len - t0);
+      const bool last = t0 + R == prompt_len;
+      GatherArgs g{};
+      g.ids = d_prompt + (size_t)b * prompt_len + t0; g.R = R; g.E = m->W<char>(y.E); g.d = y.d; g.V = y.V;
+      g.x = xp; g.ldx = y.d; g.err = m->sp.err + b;
+      launch_gather_rows(dt, g, s);
+      RowMap rm{};
+      rm.mode = ROWS_PREFILL; rm.b = b; rm.t0 = t0; rm.st = m->sp;
+      for (int l = 0; l < y.L; ++l) {
+        int rc = run_layer(m, l, R, rm, xp, true, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer,
+                           sb, sh, y.S, 1, nullptr, 0, nullptr, 0);
+        if (rc) return rc;
+        if (last)
+          for (int c = 0; c < y.C; ++c)
+            if (y.ctx_l[c] == l + 1)
+              launch_copy_row(xp + (size_t)(R - 1) * y.d, ctx + ((size_t)b * y.C + c) * y.d, y.d, s);
+      }
+      if (last) launch_copy_row(xp + (size_t)(R - 1) * y.d, x + (size_t)b * y.d, y.d, s);
+    }
+  }
+  int rc = decode_tail(m, d_out_tokens, d_out_lens);
+  if (rc) return rc;
+  HIP_TRY(hipGetLastError());
+  m->steps_done = 0;
+  return HAM_OK;
+}
+
+int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens,
+                   int32_t* d_out_lens) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  if (m->steps_done < 0) return fail(HAM_ESTATE, "ham_macro_step before ham_prefill");
+  if (!d_out_tokens || !d_out_lens) return fail(HAM_EINVAL, "null output");
+  const Layout& y = m->y;
+  if (m->steps_done >= y.steps) return fail(HAM_ECAP, "max_steps (%d) reached", y.steps);
+  if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
+  if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
+  const int dt = dtype_of(m);
+  hipStream_t s = m->s;
+  const int B = m->batch;
+  m->has_teacher = d_teacher != nullptr;
+  float* x = m->WS<float>(y.x);
+  MacroArgs ma{};
+  ma.st = m->sp; ma.B = B; ma.d = y.d; ma.G = y.G; ma.E = m->W<char>(y.E); ma.P = m->W<char>(y.Pe); ma.x = x;
+  ma.ldx = y.d; ma.emb_in = m->WS<char>(y.emb_in); ma.forced_in = d_forced_lens; ma.teacher_in = d_teacher;
+  ma.out_tokens = d_out_tokens; ma.out_lens = d_out_lens;
+  launch_macro_begin(dt, ma, s);
+
+  // compositional embedder (Sec. 3.2), skipped on device unless some group has > 1 token
+  GemmArgs ga{};
+  ga.part = m->WS<float>(y.part); ga.counters = m->WS<int>(y.gctr); ga.gate = m->sp.fused; ga.gate_n = B;
+  ga.W = m->W<char>(y.Aqkv); ga.N = 3 * y.HD; ga.K = y.d; ga.X = m->WS<char>(y.emb_in); ga.ldx = y.d;
+  ga.M = 5 * B; ga.out = m->WS<float>(y.qkv); ga.ldo = 3 * y.HD;
+  if (launch_gemm(dt, EPI_F32, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "embedder gemm shape");
+  EmbedAttnArgs ea{};
+  ea.proj = m->WS<float>(y.qkv); ea.fused = m->sp.fused; ea.B = B; ea.H = y.H; ea.d = y.d; ea.hd = y.hd;
+  ea.out = m->WS<char>(y.emb_o);
+  launch_embed_attn(dt, ea, s);
+  ga.W = m->W<char>(y.Ao); ga.N = y.d; ga.K = y.HD; ga.X = m->WS<char>(y.emb_o); ga.ldx = y.HD; ga.M = B;
+  ga.out = m->WS<char>(y.emb_y); ga.ldo = y.d;
+  if (launch_gemm(dt, EPI_OP, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "embedder gemm shape");
+  ga.W = m->W<char>(y.Alin); ga.N = y.d; ga.K = y.d; ga.X = m->WS<char>(y.emb_y); ga.ldx = y.d;
+  ga.out = x; ga.ldo = y.d; ga.rowmask = m->sp.fused;
+  if (launch_gemm(dt, EPI_XMASK, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "embedder gemm shape");
+
+  // base forward: one new KV slot per running sequence
+  RowMap rm{};
+  rm.mode = ROWS_DECODE; rm.st = m->sp;
+  const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
+  const int kv_max = m->prompt_len + m->steps_done + 1;
+  const int nsplit = attn_splits(m, B, kv_max);
+  float* ctx = m->WS<float>(y.ctx);
+  for (int l = 0; l < y.L; ++l) {
+    float* co = nullptr;
+    for (int c = 0; c < y.C; ++c)
+      if (y.ctx_l[c] == l + 1) co = ctx + (size_t)c * y.d;
+    int rc = run_layer(m, l, B, rm, x, false, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer, sb,
+                       sh, y.S, nsplit, m->sp.step_on, B, co, y.C * y.d);
+    if (rc) return rc;
+  }
+  int rc = decode_tail(m, d_out_tokens, d_out_lens);
+  if (rc) return rc;
+  HIP_TRY(hipGetLastError());
+  m->steps_done += 1;
+  return HAM_OK;
+}
+
+int ham_kv_stats(ham_model* m, ham_kv_stats_t* h_out) {
+  if (!m || !h_out) return fail(HAM_EINVAL, "null argument");
+  if (m->steps_done < 0) return fail(HAM_ESTATE, "ham_kv_stats before ham_prefill");
+  HIP_TRY(hipStreamSynchronize(m->s));
+  const int B = m->batch;
+  std::vector<int> kv(B), em(B), gr(B), dn(B), hist(5 * B), err(B);
+  HIP_TRY(hipMemcpy(kv.data(), m->sp.kv_len, 4 * B, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(em.data(), m->sp.emitted, 4 * B, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(gr.data(), m->sp.groups, 4 * B, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(dn.data(), m->sp.done, 4 * B, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(hist.data(), m->sp.hist, 20 * B, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(err.data(), m->sp.err, 4 * B, hipMemcpyDeviceToHost));
+  for (int b = 0; b < B; ++b) {
+    ham_kv_stats_t& o = h_out[b];
+    o.kv_len = kv[b];
+    o.prompt_slots = m->prompt_len;
+    o.gen_slots = kv[b] - m->prompt_len;
+    o.tokens = em[b];
+    o.groups = gr[b];
+    o.done = dn[b];
+    for (int j = 0; j < 5; ++j) o.len_hist[j] = hist[5 * b + j];
+    o.device_error = err[b];
+  }
+  return HAM_OK;
+}
+
+int ham_set_debug(ham_model* m, void* d_buf, size_t bytes) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  const Layout& y = m->y;
+  if (d_buf && bytes < (size_t)4 * y.B * (y.V + y.d + 1) * 4) return fail(HAM_ENOMEM, "debug buffer too small");
+  m->dbg = (float*)d_buf;
+  return HAM_OK;
+}
+
+int ham_steps_done(const ham_model* m) { return m ? m->steps_done : -1; }
+
+void ham_destroy(ham_model* m) { delete m; }
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+// Internal interfaces between the host orchestration (ham.cpp) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ham {
+
+// ---------------------------------------------------------------- per-sequence state
+// Structure-of-arrays in the state buffer, each int32 [max_batch] (grp_tok, teacher:
+// [max_batch][4], hist: [max_batch][5]).
+struct SeqPtrs {
+  int* kv_len;     // base KV slots held
+  int* pos_last;   // RoPE position of the newest base input
+  int* cur_pos;    // position of this step's base input
+  int* cur_slot;   // KV slot written by this step
+  int* emitted;    // tokens emitted so far
+  int* budget;     // token budget (0 = none)
+  int* done;       // budget spent
+  int* groups;     // groups emitted
+  int* hist;       // [B][5] group-length histogram
+  int* step_on;    // sequence runs this macro-step
+  int* fused;      // this step's input is a fused group (n > 1)
+  int* active;     // still waiting for the next micro decision
+  int* grp_n;      // tokens in the current group
+  int* grp_tok;    // [B][4] current group
+  int* forced;     // forced length for this step (FORCED mode)
+  int* teacher;    // [B][4] teacher tokens for this step
+  int* err;        // device-side bounds-check flags
+};
+
+// how the rows of a launch map onto sequences, KV slots and positions
+enum RowMode { ROWS_PREFILL = 0, ROWS_DECODE = 1, ROWS_MICRO1 = 2, ROWS_MICROK = 3 };
+struct RowMap {
+  int mode;
+  int b;        // PREFILL: the sequence
+  int t0;       // PREFILL: slot/position of row 0
+  int C;        // MICRO*: context rows
+  int k;        // MICROK: micro step index (>= 2)
+  SeqPtrs st;
+};
+
+// ---------------------------------------------------------------- GEMM
+enum EpiKind { EPI_F32 = 0, EPI_OP = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_ARGMAX = 4, EPI_XMASK = 5 };
+
+struct DecideArgs {
+  SeqPtrs st;
+  int B, k, mode, stop_id, G, V, has_teacher;
+  float tau;
+  int* out_tokens;   // [B][4]
+  int* out_lens;     // [B]
+  float* dbg_logits; // [B][V] for this k, or null
+  float* dbg_stop;   // [B] for this k, or null
+  float* stop_buf;   // [B] stop logits (workspace)
+  float* best_val;   // [n_wg][B] argmax partials
+  int* best_idx;
+  int* any_active;   // unused placeholder for future fusion
+};
+
+struct GemmArgs {
+  const void* W; int N, K;         // W [N][K] row-major (storage type), N % 32 == 0
+  const void* X; int ldx; int M;   // X [M][ldx] (storage type)
+  void* out; int ldo;              // destination (see EpiKind)
+  float* ctx; int ldctx;           // RESID: copy of updated rows (optional)
+  const int* rowmask;              // XMASK: rows to store
+  const int* gate; int gate_n;     // launch does nothing unless a gate flag is set
+  float* part; int* counters; int nsplit;  // split-K partials / last-arriver counters
+  DecideArgs dec;                  // ARGMAX only
+};
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  const void* q; int ldq;          // q [R][H*hd] (storage type), RoPE applied
+  const void* K; const void* VT;   // K [b][Hkv][S][hd], VT [b][Hkv][hd][S]
+  long long sb, sh;                // element strides per sequence and per kv head (both caches)
+  int S;                           // slot capacity (row length of VT)
+  int H, Hkv, hd, R, nsplit;
+  void* o; int ldo;                // o [R][H*hd] (storage type)
+  float* part; int* counters;      // split partials [R][Hkv][nsplit][grp][hd+2]
+  RowMap rm;
+  const int* gate; int gate_n;
+};
+
+// ---------------------------------------------------------------- launchers
+typedef hipStream_t Stream;
+int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s);
+int launch_attn_decode(int dtype, const AttnArgs& a, Stream s);
+int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s);
+
+struct RopeArgs {
+  const float* qkv; int ldqkv, R;  // [R][(H+2Hkv)hd] fp32 projections
+  void* q; int ldq;                // out q [R][H*hd]
+  void* K; void* VT; long long sb, sh; int S;
+  int H, Hkv, hd;
+  const float* cos_t; const float* sin_t;  // [max_pos][hd/2]
+  int max_pos;
+  RowMap rm;
+  const int* gate; int gate_n;
+};
+int launch_rope_append(int dtype, const RopeArgs& a, Stream s);
+
+struct NormArgs {
+  const float* x; int ldx; int row_stride, row_off;  // input row r = x[(r*row_stride+row_off)*ldx]
+  const float* g; int d, R; float eps;
+  void* out; int ldo;                                 // storage-type output
+  float* hid; int ldh;                                // optional fp32 copy of the normed rows
+  const int* gate; int gate_n;
+};
+int launch_rmsnorm(int dtype, const NormArgs& a, Stream s);
+
+}  // namespace ham

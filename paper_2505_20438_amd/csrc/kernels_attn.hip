@@ -1,0 +1,255 @@
+// Attention over the smashed KV cache (one slot per fused group, Sec. 3.1).
+//
+// Cache layout per layer: K [seq][kv_head][slot][hd] and V stored d-major,
+// VT [seq][kv_head][hd][slot], so that both products are matrix-core
+// contractions fed by 16-byte contiguous loads:
+//   S^T = K Q^T   (A = K rows, B = Q^T)  and  O = P V  (A = P, B = VT rows).
+// The rows of the K operand are permuted so that the score tile lands in the
+// registers exactly where the P operand of the next product needs it (lane
+// l holds the probabilities of row l & 15 for the slot slice of lane group
+// l >> 4), so no data moves between the two products.
+//
+// k_attn_decode: one wave per (query row, kv head, slot split).  The rows of
+//   the matrix products are the q-heads sharing the kv head (GQA).  Splits are
+//   combined with the log-sum-exp rule by the last wave to finish, in a fixed
+//   order.  Used for base decode (ragged kv_len per sequence) and the micro
+//   decoder's local cache.
+// k_attn_prefill: four waves of 16 consecutive query rows of one head, causal.
+//
+// Softmax statistics are fp32.  For bf16 caches the probabilities enter the
+// bf16 product as a hi + lo pair (about 16 significant bits).
+#include "device_common.h"
+#include "ham_internal.h"
+#include "rows.h"
+
+namespace ham {
+
+template <typename T> struct PFrag;
+template <> struct PFrag<bf16> {
+  // probabilities of one lane (8 slots) -> A-operand fragments (hi, lo)
+  static __device__ __forceinline__ void make(const float* p, u4& hi, u4& lo) {
+    float r[8];
+    hi = pack_frag_bf16(p);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t w = (e & 1) ? (hi[e >> 1] >> 16) : (hi[e >> 1] & 0xFFFFu);
+      r[e] = p[e] - bf2f((bf16)w);
+    }
+    lo = pack_frag_bf16(r);
+  }
+  static constexpr bool TWO = true;
+};
+template <> struct PFrag<float> {
+  static __device__ __forceinline__ void make(const float* p, u4& hi, u4& lo) {
+    hi = u4{__float_as_uint(p[0]), __float_as_uint(p[1]), __float_as_uint(p[2]), __float_as_uint(p[3])};
+    lo = hi;
+  }
+  static constexpr bool TWO = false;
+};
+
+// One key block of KB slots starting at `base`: scores for the 16 operand rows
+// (lane: row r16, slots base + g*KB/4 + e), online-softmax update of (m, l, o).
+// `limit_of_row` gives, for this lane's row, the first slot it may not see.
+template <typename T, int HD>
+__device__ __forceinline__ void attn_block(const T* Kb, const T* Vb, int S, int base, int limit,
+                                           const u4* qf, float scale, float& mrun, float& lrun,
+                                           f4* o) {
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16, TT = KB / 16;
+  const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+  float sc[KB / 4];
+#pragma unroll
+  for (int t = 0; t < TT; ++t) {
+    const int slot = base + (r16 >> 2) * (KB / 4) + 4 * t + (r16 & 3);
+    const T* kp = Kb + (size_t)slot * HD + g * EPL;
+    f4 s = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int f = 0; f < NF; ++f) Frag<T>::mma(s, ld16_stream(kp + f * KB), qf[f]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int sl = base + g * (KB / 4) + 4 * t + i;
+      sc[4 * t + i] = sl < limit ? s[i] * scale : -INFINITY;
+    }
+  }
+  float bm = sc[0];
+#pragma unroll
+  for (int e = 1; e < KB / 4; ++e) bm = fmaxf(bm, sc[e]);
+  bm = fmaxf(bm, __shfl_xor(bm, 16, WAVE));
+  bm = fmaxf(bm, __shfl_xor(bm, 32, WAVE));
+  const float mnew = fmaxf(mrun, bm);
+  const float alpha = (mrun == -INFINITY) ? 0.f : __expf(mrun - mnew);
+  float p[KB / 4];
+  float ps = 0.f;
+#pragma unroll
+  for (int e = 0; e < KB / 4; ++e) {
+    p[e] = (sc[e] == -INFINITY) ? 0.f : __expf(sc[e] - mnew);
+    ps += p[e];
+  }
+  ps += __shfl_xor(ps, 16, WAVE);
+  ps += __shfl_xor(ps, 32, WAVE);
+  lrun = lrun * alpha + ps;
+  mrun = mnew;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float ai = __shfl(alpha, 4 * g + i, WAVE);
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) o[dt][i] *= ai;
+  }
+  u4 phi, plo;
+  PFrag<T>::make(p, phi, plo);
+  const T* vp = Vb + (size_t)r16 * S + base + g * (KB / 4);
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) {
+    const u4 vf = ld16_stream(vp + (size_t)dt * 16 * S);
+    Frag<T>::mma(o[dt], phi, vf);
+    if constexpr (PFrag<T>::TWO) Frag<T>::mma(o[dt], plo, vf);
+  }
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16;
+  __shared__ int sh_flag;
+  const int lane = threadIdx.x, r16 = lane & 15, g = lane >> 4;
+  const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
+  const int grp = a.H / a.Hkv;
+  const RowInfo ri = row_info(a.rm, r);
+  const int nval = ri.enabled ? ri.n_valid : 0;
+  int chunk = (nval + a.nsplit - 1) / a.nsplit;
+  chunk = (chunk + KB - 1) / KB * KB;
+  const int s0 = split * chunk;
+  const int s1 = min(nval, s0 + chunk);
+  const T* Kb = (const T*)a.K + ri.b * a.sb + kvh * a.sh;
+  const T* Vb = (const T*)a.VT + ri.b * a.sb + kvh * a.sh;
+  u4 qf[NF];
+  const T* qp = (const T*)a.q + (size_t)r * a.ldq + (size_t)(kvh * grp + r16) * HD + g * EPL;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) qf[f] = (r16 < grp) ? ld16(qp + f * KB) : zero16();
+  f4 o[ND];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.f;
+  const float scale = 1.0f / sqrtf((float)HD);
+  for (int base = s0; base < s1; base += KB) attn_block<T, HD>(Kb, Vb, a.S, base, s1, qf, scale, mrun, lrun, o);
+
+  if (a.nsplit == 1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = 4 * g + i;
+      const float lj = __shfl(lrun, j & 15, WAVE);
+      if (j < grp) {
+        T* op = (T*)a.o + (size_t)r * a.ldo + (size_t)(kvh * grp + j) * HD + r16;
+        const float inv = lj > 0.f ? 1.0f / lj : 0.f;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) op[dt * 16] = from_f<T>(o[dt][i] * inv);
+      }
+    }
+    return;
+  }
+  // publish (m, l, O) of this split: part[r][kvh][split][j][HD + 2]
+  const size_t rec = HD + 2;
+  float* pb = a.part + (((size_t)r * a.Hkv + kvh) * a.nsplit) * grp * rec;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = 4 * g + i;
+    if (j < grp) {
+      float* pj = pb + ((size_t)split * grp + j) * rec;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) pj[dt * 16 + r16] = o[dt][i];
+    }
+  }
+  if (r16 < grp && g == 0) {
+    float* pj = pb + ((size_t)split * grp + r16) * rec;
+    pj[HD] = mrun;
+    pj[HD + 1] = lrun;
+  }
+  if (!last_arriver(a.counters + r * a.Hkv + kvh, a.nsplit, &sh_flag)) return;
+  for (int j = 0; j < grp; ++j) {
+    float M = -INFINITY;
+    for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, pb[((size_t)s * grp + j) * rec + HD]);
+    T* op = (T*)a.o + (size_t)r * a.ldo + (size_t)(kvh * grp + j) * HD;
+    for (int d = lane; d < HD; d += 64) {
+      float L = 0.f, O = 0.f;
+      if (M != -INFINITY) {
+        for (int s = 0; s < a.nsplit; ++s) {
+          const float* ps = pb + ((size_t)s * grp + j) * rec;
+          const float ms = ps[HD];
+          const float wgt = ms == -INFINITY ? 0.f : __expf(ms - M);
+          L += wgt * ps[HD + 1];
+          O += wgt * ps[d];
+        }
+      }
+      op[d] = from_f<T>(L > 0.f ? O / L : 0.f);
+    }
+  }
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
+  const int h = blockIdx.y;
+  const int grp = a.H / a.Hkv, kvh = h / grp;
+  const int row0 = blockIdx.x * 64 + w * 16;
+  if (row0 >= a.R) return;
+  const RowInfo r0 = row_info(a.rm, row0);
+  const T* Kb = (const T*)a.K + r0.b * a.sb + kvh * a.sh;
+  const T* Vb = (const T*)a.VT + r0.b * a.sb + kvh * a.sh;
+  const int qrow = row0 + r16;
+  const bool qok = qrow < a.R;
+  u4 qf[NF];
+  const T* qp = (const T*)a.q + (size_t)(qok ? qrow : row0) * a.ldq + (size_t)h * HD + g * EPL;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) qf[f] = qok ? ld16(qp + f * KB) : zero16();
+  // causal: row with slot s sees slots [0, s]; rows past the chunk see nothing
+  const int limit = qok ? r0.slot + r16 + 1 : 0;
+  const int wave_end = r0.slot + min(15, a.R - 1 - row0) + 1;
+  f4 o[ND];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.f;
+  const float scale = 1.0f / sqrtf((float)HD);
+  for (int base = 0; base < wave_end; base += KB) {
+    // per-lane limit: the score mask uses this lane's query row (r16)
+    attn_block<T, HD>(Kb, Vb, a.S, base, limit, qf, scale, mrun, lrun, o);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = 4 * g + i;  // query row within the wave
+    const float lj = __shfl(lrun, j, WAVE);
+    if (row0 + j < a.R) {
+      T* op = (T*)a.o + (size_t)(row0 + j) * a.ldo + (size_t)h * HD + r16;
+      const float inv = lj > 0.f ? 1.0f / lj : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) op[dt * 16] = from_f<T>(o[dt][i] * inv);
+    }
+  }
+}
+
+template <typename T>
+static int decode_t(const AttnArgs& a, Stream s) {
+  dim3 grid(a.nsplit, a.Hkv, a.R);
+  if (a.hd == 64) hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64), 0, s, a);
+  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64), 0, s, a);
+  else return -1;
+  return 0;
+}
+template <typename T>
+static int prefill_t(const AttnArgs& a, Stream s) {
+  dim3 grid((a.R + 63) / 64, a.H);
+  if (a.hd == 64) hipLaunchKernelGGL((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, a);
+  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, a);
+  else return -1;
+  return 0;
+}
+
+int launch_attn_decode(int dtype, const AttnArgs& a, Stream s) {
+  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 16 || a.S % 64 != 0) return -1;
+  return dtype == 1 ? decode_t<bf16>(a, s) : decode_t<float>(a, s);
+}
+int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s) {
+  if (a.H % a.Hkv != 0 || a.S % 64 != 0 || a.rm.mode != ROWS_PREFILL) return -1;
+  return dtype == 1 ? prefill_t<bf16>(a, s) : prefill_t<float>(a, s);
+}
+
+}  // namespace ham

@@ -1,0 +1,58 @@
+// Argument blocks and launchers of the small kernels (kernels_misc.hip).
+#pragma once
+#include "ham_internal.h"
+
+namespace ham {
+
+struct MacroArgs {
+  SeqPtrs st;
+  int B, d, G;
+  const void* E; const void* P;     // token and relative-position embeddings
+  float* x; int ldx;                // residual rows [B][d] (bypass rows written here)
+  void* emb_in;                     // [B][5][d] embedder GEMM rows (query, tokens 0..3)
+  const int* forced_in;             // [B] or null
+  const int* teacher_in;            // [B][4] or null
+  int* out_tokens; int* out_lens;
+};
+
+struct EmbedAttnArgs {
+  const float* proj;                // [B*5][3d]
+  const int* fused;                 // [B] group size when fused, else 0
+  int B, H, d, hd;
+  void* out;                        // [B][H*hd] storage type
+};
+
+struct PrefillArgs {
+  SeqPtrs st;
+  int B, P, G;
+  const int* forced_in; const int* teacher_in;
+  int* out_tokens; int* out_lens;
+};
+
+struct GatherArgs {
+  const int* ids; int R; const void* E; int d, V; float* x; int ldx;
+  int* err;                         // set (bit 2) if an id is out of range
+};
+
+struct MicroPrepArgs {
+  SeqPtrs st;
+  int B, C, k, d;
+  const float* ctx;                 // [B][C][d]
+  const void* E;
+  float* x;                         // [rows][d]
+};
+
+struct GenArgs {
+  void* dst; int rows, cols; long long row_off; int interleave; uint64_t key;
+};
+
+void launch_macro_begin(int dtype, const MacroArgs& a, Stream s);
+void launch_embed_attn(int dtype, const EmbedAttnArgs& a, Stream s);
+void launch_prefill_begin(const PrefillArgs& a, Stream s);
+void launch_gather_rows(int dtype, const GatherArgs& a, Stream s);
+void launch_copy_row(const float* src, float* dst, int d, Stream s);
+void launch_micro_prep(int dtype, const MicroPrepArgs& a, Stream s);
+void launch_gen_normal(int dtype, const GenArgs& a, Stream s);
+void launch_fill_f32(float* p, long long n, float v, Stream s);
+
+}  // namespace ham

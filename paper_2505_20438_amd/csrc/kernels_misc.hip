@@ -1,0 +1,318 @@
+// Elementwise and bookkeeping kernels of the decode loop: RMSNorm, RoPE with
+// the KV append, the compositional embedder's small pieces, the macro-step and
+// prefill set-up of per-sequence state, the micro-decoder input rows, and the
+// seeded weight initialiser.
+#include <math.h>
+
+#include "device_common.h"
+#include "ham_internal.h"
+#include "kernels_misc.h"
+#include "rows.h"
+
+namespace ham {
+
+// ---------------------------------------------------------------- RMSNorm
+// out[r] = g * x / sqrt(mean(x^2) + eps), rounded to the storage type (the GEMM operand)
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  __shared__ float sh[4];
+  const int r = blockIdx.x;
+  const float* x = a.x + (size_t)(r * a.row_stride + a.row_off) * a.ldx;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
+  ss = block_sum256(ss, sh);
+  const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+  T* o = (T*)a.out + (size_t)r * a.ldo;
+  for (int i = threadIdx.x; i < a.d; i += 256) {
+    const float v = x[i] * inv * a.g[i];
+    o[i] = from_f<T>(v);
+    if (a.hid) a.hid[(size_t)r * a.ldh + i] = v;
+  }
+}
+
+int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
+  if (a.R <= 0) return 0;
+  if (dtype == 1) hipLaunchKernelGGL((k_rmsnorm<bf16>), dim3(a.R), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k_rmsnorm<float>), dim3(a.R), dim3(256), 0, s, a);
+  return 0;
+}
+
+// ---------------------------------------------------------------- RoPE + KV append
+// Rotate-half RoPE of q and k at the row's position; q -> q buffer, k -> K cache
+// slot, v -> VT cache column (d-major).  One block per (head of q|k|v, row).
+template <typename T>
+__global__ __launch_bounds__(64) void k_rope_append(RopeArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  const int hh = blockIdx.x, r = blockIdx.y;
+  const int half = a.hd / 2;
+  const RowInfo ri = row_info(a.rm, r);
+  const float* src = a.qkv + (size_t)r * a.ldqkv + (size_t)hh * a.hd;
+  const bool okpos = ri.pos >= 0 && ri.pos < a.max_pos;
+  const bool okslot = ri.slot >= 0 && ri.slot < a.S;
+  if (!(okpos && okslot)) {
+    if (threadIdx.x == 0 && ri.enabled) atomicOr(a.rm.st.err + ri.b, 1);
+    return;
+  }
+  for (int i = threadIdx.x; i < half; i += 64) {
+    const float x1 = src[i], x2 = src[i + half];
+    if (hh < a.H + a.Hkv) {
+      const float c = a.cos_t[(size_t)ri.pos * half + i], sn = a.sin_t[(size_t)ri.pos * half + i];
+      const float y1 = x1 * c - x2 * sn, y2 = x2 * c + x1 * sn;
+      if (hh < a.H) {
+        T* q = (T*)a.q + (size_t)r * a.ldq + (size_t)hh * a.hd;
+        q[i] = from_f<T>(y1);
+        q[i + half] = from_f<T>(y2);
+      } else if (ri.enabled) {
+        T* k = (T*)a.K + ri.b * a.sb + (hh - a.H) * a.sh + (size_t)ri.slot * a.hd;
+        k[i] = from_f<T>(y1);
+        k[i + half] = from_f<T>(y2);
+      }
+    } else if (ri.enabled) {
+      T* v = (T*)a.VT + ri.b * a.sb + (hh - a.H - a.Hkv) * a.sh + ri.slot;
+      v[(size_t)i * a.S] = from_f<T>(x1);
+      v[(size_t)(i + half) * a.S] = from_f<T>(x2);
+    }
+  }
+}
+
+int launch_rope_append(int dtype, const RopeArgs& a, Stream s) {
+  if (a.R <= 0) return 0;
+  dim3 grid(a.H + 2 * a.Hkv, a.R);
+  if (dtype == 1) hipLaunchKernelGGL((k_rope_append<bf16>), grid, dim3(64), 0, s, a);
+  else hipLaunchKernelGGL((k_rope_append<float>), grid, dim3(64), 0, s, a);
+  return 0;
+}
+
+// ---------------------------------------------------------------- macro-step set-up
+// For each sequence: consume the previous group (fuse it or bypass), advance the
+// position by the group size (the fused input sits at its last token's position,
+// Sec. 3.2), take the next KV slot, and open a new group.
+template <typename T>
+__global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
+  __shared__ int tok[4];
+  __shared__ int sn, son;
+  const int b = blockIdx.x;
+  const SeqPtrs& st = a.st;
+  if (threadIdx.x == 0) {
+    const int on = st.done[b] ? 0 : 1;
+    const int n = st.grp_n[b];
+    sn = n;
+    son = on;
+    for (int j = 0; j < 4; ++j) tok[j] = j < n ? st.grp_tok[b * 4 + j] : 0;
+  }
+  __syncthreads();
+  const int n = sn, on = son;
+  const int d = a.d;
+  const T* E = (const T*)a.E;
+  const T* P = (const T*)a.P;
+  if (on && n == 1) {
+    for (int i = threadIdx.x; i < d; i += 256) a.x[(size_t)b * a.ldx + i] = to_f<T>(E[(size_t)tok[0] * d + i]);
+  } else if (on && n > 1) {
+    // e_j = E[t_j] + P[j]; query = mean_j e_j; rows of the embedder's projection GEMM
+    T* rows = (T*)a.emb_in + (size_t)b * 5 * d;
+    for (int i = threadIdx.x; i < d; i += 256) {
+      float sum = 0.f;
+      for (int j = 0; j < 4; ++j) {
+        float e = 0.f;
+        if (j < n) {
+          e = to_f<T>(E[(size_t)tok[j] * d + i]) + to_f<T>(P[(size_t)j * d + i]);
+          sum += e;
+        }
+        rows[(size_t)(1 + j) * d + i] = from_f<T>(e);
+      }
+      rows[i] = from_f<T>(sum / (float)n);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    st.step_on[b] = on;
+    st.fused[b] = (on && n > 1) ? n : 0;
+    if (on) {
+      const int p = st.pos_last[b] + n;
+      st.pos_last[b] = p;
+      st.cur_pos[b] = p;
+      st.cur_slot[b] = st.kv_len[b];
+      st.kv_len[b] += 1;
+    }
+    st.forced[b] = a.forced_in ? a.forced_in[b] : a.G;
+    for (int j = 0; j < 4; ++j) {
+      st.teacher[b * 4 + j] = a.teacher_in ? a.teacher_in[b * 4 + j] : 0;
+      a.out_tokens[b * 4 + j] = -1;
+    }
+    a.out_lens[b] = 0;
+    st.grp_n[b] = 0;
+    st.active[b] = on;
+  }
+}
+
+// Embedder attention over the <= 4 token rows of a fused group: per head, the
+// mean query attends to the rows' keys (Sec. 3.2).  proj = [B*5][3d] fp32 rows
+// (row 0 query, rows 1..4 tokens; columns Q | K | V).
+template <typename T>
+__global__ __launch_bounds__(64) void k_embed_attn(EmbedAttnArgs a) {
+  const int b = blockIdx.x, h = blockIdx.y;
+  const int n = a.fused[b];
+  if (n < 2) return;
+  const int hd = a.hd, HD = a.H * a.hd;  // proj row: Q | K | V blocks of H*hd each
+  const float* base = a.proj + (size_t)b * 5 * 3 * HD;
+  const float* Q = base + (size_t)h * hd;
+  __shared__ float w[4];
+  if (threadIdx.x < 4) {
+    const int j = threadIdx.x;
+    float s = -INFINITY;
+    if (j < n) {
+      const float* K = base + (size_t)(1 + j) * 3 * HD + HD + (size_t)h * hd;
+      s = 0.f;
+      for (int i = 0; i < hd; ++i) s += Q[i] * K[i];
+      s *= 1.0f / sqrtf((float)hd);
+    }
+    w[j] = s;
+  }
+  __syncthreads();
+  float m = fmaxf(fmaxf(w[0], w[1]), fmaxf(w[2], w[3]));
+  float e[4], sum = 0.f;
+  for (int j = 0; j < 4; ++j) {
+    e[j] = j < n ? expf(w[j] - m) : 0.f;
+    sum += e[j];
+  }
+  T* o = (T*)a.out + (size_t)b * HD + (size_t)h * hd;
+  for (int i = threadIdx.x; i < hd; i += 64) {
+    float acc = 0.f;
+    for (int j = 0; j < n; ++j) acc += e[j] * base[(size_t)(1 + j) * 3 * HD + 2 * HD + (size_t)h * hd + i];
+    o[i] = from_f<T>(acc / sum);
+  }
+}
+
+// ---------------------------------------------------------------- prefill set-up
+__global__ void k_prefill_begin(PrefillArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.B) return;
+  const SeqPtrs& st = a.st;
+  st.kv_len[b] = a.P;
+  st.pos_last[b] = a.P - 1;
+  st.cur_pos[b] = a.P - 1;
+  st.cur_slot[b] = a.P - 1;
+  st.emitted[b] = 0;
+  st.done[b] = 0;
+  st.groups[b] = 0;
+  for (int j = 0; j < 5; ++j) st.hist[b * 5 + j] = 0;
+  st.step_on[b] = 1;
+  st.fused[b] = 0;
+  st.grp_n[b] = 0;
+  st.active[b] = 1;
+  st.err[b] = 0;
+  st.forced[b] = a.forced_in ? a.forced_in[b] : a.G;
+  for (int j = 0; j < 4; ++j) {
+    st.teacher[b * 4 + j] = a.teacher_in ? a.teacher_in[b * 4 + j] : 0;
+    a.out_tokens[b * 4 + j] = -1;
+  }
+  a.out_lens[b] = 0;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gather_rows(GatherArgs a) {
+  const int r = blockIdx.x;
+  int t = a.ids[r];
+  if (t < 0 || t >= a.V) {  // caller-provided id out of range: flag it, read row 0
+    if (threadIdx.x == 0) atomicOr(a.err, 2);
+    t = 0;
+  }
+  const T* E = (const T*)a.E;
+  for (int i = threadIdx.x; i < a.d; i += 256) a.x[(size_t)r * a.ldx + i] = to_f<T>(E[(size_t)t * a.d + i]);
+}
+
+__global__ __launch_bounds__(256) void k_copy_row(const float* src, float* dst, int d) {
+  for (int i = threadIdx.x; i < d; i += 256) dst[i] = src[i];
+}
+
+// micro-decoder inputs: step 1 = [ctx_1..ctx_C, E[t_0]] per sequence, step k = E[t_{k-1}]
+template <typename T>
+__global__ __launch_bounds__(256) void k_micro_prep(MicroPrepArgs a) {
+  const int r = blockIdx.x;
+  const int per = a.k == 1 ? a.C + 1 : 1;
+  const int b = r / per, c = r % per;
+  if (!a.st.active[b]) return;
+  float* x = a.x + (size_t)r * a.d;
+  const T* E = (const T*)a.E;
+  if (a.k == 1 && c < a.C) {
+    const float* src = a.ctx + ((size_t)b * a.C + c) * a.d;
+    for (int i = threadIdx.x; i < a.d; i += 256) x[i] = src[i];
+  } else {
+    const int t = a.st.grp_tok[b * 4 + a.k - 1];
+    for (int i = threadIdx.x; i < a.d; i += 256) x[i] = to_f<T>(E[(size_t)t * a.d + i]);
+  }
+}
+
+// ---------------------------------------------------------------- weight generator
+// SplitMix64 (Steele, Lea, Flood 2014): i-th output of the stream seeded with s.
+__device__ __forceinline__ uint64_t sm64(uint64_t s, uint64_t i) {
+  uint64_t z = s + (i + 1ull) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Box-Muller (cosine branch) in float64, scaled by 0.02, rounded to fp32 then T.
+template <typename T>
+__global__ __launch_bounds__(256) void k_gen_normal(GenArgs a) {
+  const long long count = (long long)a.rows * a.cols;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < count; i += (long long)gridDim.x * 256) {
+    const uint64_t r1 = sm64(a.key, 2ull * (uint64_t)i), r2 = sm64(a.key, 2ull * (uint64_t)i + 1ull);
+    const double u1 = ((double)(r1 >> 11) + 1.0) * 0x1p-53;
+    const double u2 = (double)(r2 >> 11) * 0x1p-53;
+    const double rad = sqrt(-2.0 * log(u1));
+    const double ang = (2.0 * 3.141592653589793) * u2;
+    const double nv = rad * cos(ang);
+    const float v = (float)(nv * 0.02);
+    const long long row = i / a.cols, col = i % a.cols;
+    long long drow = row + a.row_off;
+    if (a.interleave) drow = 32 * (row / 16) + (row % 16) + (a.interleave == 2 ? 16 : 0) + a.row_off;
+    ((T*)a.dst)[drow * a.cols + col] = from_f<T>(v);
+  }
+}
+
+__global__ void k_fill_f32(float* p, long long n, float v) {
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long long)gridDim.x * 256) p[i] = v;
+}
+
+// ---------------------------------------------------------------- launchers
+#define HAM_T_LAUNCH(dtype, kern, grid, block, s, arg)                           \
+  do {                                                                           \
+    if ((dtype) == 1) hipLaunchKernelGGL((kern<bf16>), grid, block, 0, s, arg);  \
+    else hipLaunchKernelGGL((kern<float>), grid, block, 0, s, arg);              \
+  } while (0)
+
+void launch_macro_begin(int dtype, const MacroArgs& a, Stream s) {
+  HAM_T_LAUNCH(dtype, k_macro_begin, dim3(a.B), dim3(256), s, a);
+}
+void launch_embed_attn(int dtype, const EmbedAttnArgs& a, Stream s) {
+  HAM_T_LAUNCH(dtype, k_embed_attn, dim3(a.B, a.H), dim3(64), s, a);
+}
+void launch_prefill_begin(const PrefillArgs& a, Stream s) {
+  hipLaunchKernelGGL(k_prefill_begin, dim3((a.B + 255) / 256), dim3(256), 0, s, a);
+}
+void launch_gather_rows(int dtype, const GatherArgs& a, Stream s) {
+  HAM_T_LAUNCH(dtype, k_gather_rows, dim3(a.R), dim3(256), s, a);
+}
+void launch_copy_row(const float* src, float* dst, int d, Stream s) {
+  hipLaunchKernelGGL(k_copy_row, dim3(1), dim3(256), 0, s, src, dst, d);
+}
+void launch_micro_prep(int dtype, const MicroPrepArgs& a, Stream s) {
+  const int rows = a.k == 1 ? a.B * (a.C + 1) : a.B;
+  HAM_T_LAUNCH(dtype, k_micro_prep, dim3(rows), dim3(256), s, a);
+}
+void launch_gen_normal(int dtype, const GenArgs& a, Stream s) {
+  const long long count = (long long)a.rows * a.cols;
+  long long blocks = (count + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  HAM_T_LAUNCH(dtype, k_gen_normal, dim3((unsigned)blocks), dim3(256), s, a);
+}
+void launch_fill_f32(float* p, long long n, float v, Stream s) {
+  long long blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_fill_f32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+}
+
+}  // namespace ham

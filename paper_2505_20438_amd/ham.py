@@ -1,0 +1,217 @@
+"""Thin ctypes binding of libham (include/ham.h): argument marshalling only.
+
+Every step of the decode loop runs in the library's HIP kernels; this module
+passes device pointers (from torch tensors) and the caller's HIP stream.
+It fails loudly when the compiled library is missing: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libham.so")
+
+HAM_OK, HAM_EINVAL, HAM_ENOMEM, HAM_EHIP, HAM_ESTATE, HAM_ECAP = 0, -1, -2, -3, -4, -5
+HAM_F32, HAM_BF16 = 0, 1
+HAM_STOP_HEAD, HAM_STOP_TOKEN, HAM_STOP_FORCED = 0, 1, 2
+
+EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
+            "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
+            "ham_tensor_info", "ham_last_error", "ham_destroy")
+
+
+class HamConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "vocab",
+        "micro_layers", "max_group", "stop_mode", "stop_id")] + [
+        ("stop_conf", ctypes.c_float), ("rope_theta", ctypes.c_float), ("norm_eps", ctypes.c_float),
+        ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_prompt", ctypes.c_int32),
+        ("max_steps", ctypes.c_int32)]
+
+
+class HamKvStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "kv_len", "prompt_slots", "gen_slots", "tokens", "groups", "done")] + [
+        ("len_hist", ctypes.c_int32 * 5), ("device_error", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        d = {n: getattr(self, n) for n, _ in self._fields_ if n != "len_hist"}
+        d["len_hist"] = list(self.len_hist)
+        return d
+
+
+class HamError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libham error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libham.so; raises if it has not been built (no fallback path exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is missing: build it with `python -m paper_2505_20438_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, SZ, U64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.c_uint64
+    cfgp = ctypes.POINTER(HamConfig)
+    for n in ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes"):
+        getattr(lib, n).argtypes = [cfgp]
+        getattr(lib, n).restype = SZ
+    lib.ham_init_weights.argtypes = [cfgp, U64, P, SZ, P, SZ, P, SZ, P, ctypes.POINTER(P)]
+    lib.ham_prefill.argtypes = [P, I32, P, I32, P, P, P, P, P]
+    lib.ham_macro_step.argtypes = [P, P, P, P, P]
+    lib.ham_kv_stats.argtypes = [P, ctypes.POINTER(HamKvStats)]
+    lib.ham_set_debug.argtypes = [P, P, SZ]
+    lib.ham_steps_done.argtypes = [P]
+    lib.ham_tensor_info.argtypes = [cfgp, I32, ctypes.POINTER(SZ), ctypes.POINTER(I32), ctypes.POINTER(I32),
+                                    ctypes.POINTER(I32)]
+    lib.ham_last_error.restype = ctypes.c_char_p
+    lib.ham_destroy.argtypes = [P]
+    lib.ham_destroy.restype = None
+    for n in ("ham_init_weights", "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug",
+              "ham_steps_done", "ham_tensor_info"):
+        getattr(lib, n).restype = I32
+    _lib = lib
+    return lib
+
+
+def _check(rc: int) -> None:
+    if rc != HAM_OK:
+        raise HamError(rc, load_library().ham_last_error().decode())
+
+
+def make_config(**kw) -> HamConfig:
+    c = HamConfig()
+    defaults = dict(max_group=4, stop_mode=HAM_STOP_FORCED, stop_id=0, stop_conf=0.5, rope_theta=500000.0,
+                    norm_eps=1e-5, dtype=HAM_BF16, max_batch=1, max_prompt=1, max_steps=0)
+    defaults.update(kw)
+    for k, v in defaults.items():
+        setattr(c, k, v)
+    return c
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def ham_weights_bytes(cfg: HamConfig) -> int:
+    return load_library().ham_weights_bytes(ctypes.byref(cfg))
+
+
+def ham_state_bytes(cfg: HamConfig) -> int:
+    return load_library().ham_state_bytes(ctypes.byref(cfg))
+
+
+def ham_workspace_bytes(cfg: HamConfig) -> int:
+    return load_library().ham_workspace_bytes(ctypes.byref(cfg))
+
+
+def ham_tensor_info(cfg: HamConfig, tensor_id: int):
+    off, rows, cols, inter = ctypes.c_size_t(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().ham_tensor_info(ctypes.byref(cfg), tensor_id, ctypes.byref(off), ctypes.byref(rows),
+                                          ctypes.byref(cols), ctypes.byref(inter)))
+    return off.value, rows.value, cols.value, inter.value
+
+
+def ham_init_weights(cfg: HamConfig, seed: int, weights, state, workspace, stream: int) -> int:
+    h = ctypes.c_void_p()
+    _check(load_library().ham_init_weights(
+        ctypes.byref(cfg), seed, weights.data_ptr(), weights.numel() * weights.element_size(), state.data_ptr(),
+        state.numel() * state.element_size(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+        stream, ctypes.byref(h)))
+    return h.value
+
+
+def ham_prefill(model: int, batch: int, prompt, prompt_len: int, max_new: Sequence[int], forced=None,
+                teacher=None, out_tokens=None, out_lens=None) -> None:
+    arr = (ctypes.c_int32 * batch)(*[int(x) for x in max_new])
+    _check(load_library().ham_prefill(model, batch, _ptr(prompt), prompt_len, arr, _ptr(forced), _ptr(teacher),
+                                      _ptr(out_tokens), _ptr(out_lens)))
+
+
+def ham_macro_step(model: int, forced=None, teacher=None, out_tokens=None, out_lens=None) -> None:
+    _check(load_library().ham_macro_step(model, _ptr(forced), _ptr(teacher), _ptr(out_tokens), _ptr(out_lens)))
+
+
+def ham_kv_stats(model: int, batch: int) -> List[dict]:
+    out = (HamKvStats * batch)()
+    _check(load_library().ham_kv_stats(model, out))
+    return [o.as_dict() for o in out]
+
+
+def ham_set_debug(model: int, buf) -> None:
+    _check(load_library().ham_set_debug(model, _ptr(buf), 0 if buf is None else buf.numel() * buf.element_size()))
+
+
+def ham_steps_done(model: int) -> int:
+    return load_library().ham_steps_done(model)
+
+
+def ham_destroy(model: int) -> None:
+    load_library().ham_destroy(model)
+
+
+class HamRuntime:
+    """Allocates the library's three buffers as torch tensors on one device and
+    binds them (``ham_init_weights``).  Device memory and the stream are torch's;
+    the computation is the library's."""
+
+    def __init__(self, cfg: HamConfig, seed: int, device: str = "cuda:0", stream=None):
+        import torch
+        self.torch = torch
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.stream = stream or torch.cuda.current_stream(self.device)
+        nb = [ham_weights_bytes(cfg), ham_state_bytes(cfg), ham_workspace_bytes(cfg)]
+        if 0 in nb:
+            raise HamError(HAM_EINVAL, "invalid configuration")
+        self.weights, self.state, self.workspace = (
+            torch.empty(n, dtype=torch.uint8, device=self.device) for n in nb)
+        self.handle = ham_init_weights(cfg, seed, self.weights, self.state, self.workspace,
+                                       self.stream.cuda_stream)
+        B = cfg.max_batch
+        self.out_tokens = torch.full((B, 4), -1, dtype=torch.int32, device=self.device)
+        self.out_lens = torch.zeros(B, dtype=torch.int32, device=self.device)
+        self.batch = 0
+
+    def prefill(self, prompt, max_new, forced=None, teacher=None):
+        self.batch = prompt.shape[0]
+        ham_prefill(self.handle, prompt.shape[0], prompt, prompt.shape[1], max_new, forced, teacher,
+                    self.out_tokens, self.out_lens)
+
+    def macro_step(self, forced=None, teacher=None):
+        ham_macro_step(self.handle, forced, teacher, self.out_tokens, self.out_lens)
+
+    def kv_stats(self):
+        return ham_kv_stats(self.handle, self.batch)
+
+    def tensor(self, tensor_id: int):
+        """A generated tensor as stored (row-major, rows in storage order)."""
+        torch = self.torch
+        off, rows, cols, inter = ham_tensor_info(self.cfg, tensor_id)
+        es = 2 if self.cfg.dtype == HAM_BF16 else 4
+        dt = torch.int16 if es == 2 else torch.float32
+        span = rows * cols if not inter else 2 * rows * cols
+        flat = self.weights[off: off + span * es].view(dt)
+        if not inter:
+            return flat.view(rows, cols)
+        blocks = flat.view(rows // 16, 2, 16, cols)
+        return blocks[:, inter - 1].reshape(rows, cols)
+
+    def close(self):
+        if self.handle:
+            ham_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

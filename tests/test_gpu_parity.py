@@ -1,0 +1,146 @@
+"""GPU parity of the decode loop against the oracle, through the C ABI.
+
+Marked ``gpu``: needs an MI355X and ``libham.so`` built in-tree.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleHam
+from synth.configs import BF16, SHAPE_1B, STOP_FORCED, STOP_HEAD, STOP_TOKEN, TINY, WORKLOADS
+from tests.gpu_util import TOL, check_decision, config_for, oracle_groups_for, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2505_20438_amd import ham
+    ham.load_library()
+    return torch
+
+
+def _runtime(shape, seed, batch, prompt, steps):
+    from paper_2505_20438_amd import ham
+    return ham.HamRuntime(config_for(shape, batch, prompt, steps), seed)
+
+
+def test_weights_match_seeded_generator(torch_cuda):
+    # the device initialiser and the shared input generator implement one definition
+    shp = TINY
+    rt = _runtime(shp, 1001, 1, 64, 8)
+    ids = [synth.T_EMBED, synth.T_RELPOS, synth.T_AQ, synth.T_AV, synth.T_ALIN, synth.T_LMHEAD, synth.T_STOP,
+           synth.layer_tensor_id(0, synth.L_WQ), synth.layer_tensor_id(1, synth.L_WG),
+           synth.layer_tensor_id(1, synth.L_WU), synth.layer_tensor_id(2, synth.L_WD)]
+    for tid in ids:
+        got = rt.tensor(tid).cpu().numpy()
+        want = synth.normal_tensor(1001, tid, got.size, bf16=False).reshape(got.shape)
+        # float64 libm differences can move a value by one fp32 ulp at a rounding boundary
+        mism = np.mean(got != want)
+        assert mism < 1e-5 and np.max(np.abs(got - want)) <= 1e-8, (tid, mism)
+
+
+def test_weights_match_generator_bf16_1b_sample(torch_cuda):
+    import torch
+    shp = SHAPE_1B
+    rt = _runtime(shp, 1002, 1, 64, 4)
+    rng = np.random.default_rng(0)
+    for tid in (synth.T_EMBED, synth.T_LMHEAD, synth.layer_tensor_id(7, synth.L_WU),
+                synth.layer_tensor_id(17, synth.L_WD)):
+        t = rt.tensor(tid)
+        rows, cols = t.shape
+        idx = rng.integers(0, rows * cols, 20000)
+        got = t.reshape(-1)[torch.from_numpy(idx).to(t.device)].cpu().numpy().view(np.uint16)
+        want = synth.normal_elements(1002, tid, idx, bf16=True)
+        assert np.mean(got != want) < 1e-4, tid
+
+
+@pytest.mark.parametrize("mode", ["c1", "head", "forced"])
+def test_tiny_fp32_free_running_exact(torch_cuda, mode):
+    # configuration 1: fp32, TOKEN stop id 1023, 64-token prompt, 128 macro-steps, no budget;
+    # plus HEAD (c = 0.5) and FORCED variants on the same weights
+    w = WORKLOADS["c1_tiny_f32"]
+    shp = w.shape
+    sched = None
+    if mode == "head":
+        shp = dataclasses.replace(shp, stop_mode=STOP_HEAD, stop_conf=0.5)
+    elif mode == "forced":
+        shp = dataclasses.replace(shp, stop_mode=STOP_FORCED)
+        sched = synth.group_schedule(w.seed_sched, 1, w.macro_steps + 1, 4)
+    prompts = synth.prompt_ids(w.seed_prompt, 1, w.prompt_len, shp.vocab)
+    om = OracleHam(shp, w.seed_weights)
+    orc = oracle_groups_for(om, prompts, [0], w.macro_steps, sched, record=True)[0]
+    rt = _runtime(shp, w.seed_weights, 1, w.prompt_len, w.macro_steps)
+    res = run_gpu(rt, prompts, [0], w.macro_steps, sched, debug_steps=6)
+    # logits and normed hidden states of the first steps within the fp32 tolerance
+    decs = {(d.step, d.k): d for d in orc.decisions}
+    for (b, step, k), lg in res.logits.items():
+        d = decs[(step, k)]
+        assert np.max(np.abs(lg - d.logits)) <= TOL[0], (step, k)
+        assert np.max(np.abs(res.hidden[(b, step, k)] - d.h)) <= TOL[0], (step, k)
+        assert abs(res.stop[(b, step, k)] - d.stop_logit) <= TOL[0], (step, k)
+    assert res.groups[0] == orc.groups
+    st = res.stats[0]
+    assert st["kv_len"] == orc.kv_len and st["gen_slots"] == w.macro_steps
+    assert st["tokens"] == orc.tokens and st["groups"] == len(orc.groups)
+    assert st["device_error"] == 0
+    assert sum(st["len_hist"]) == len(orc.groups)
+
+
+SMALL16 = dataclasses.replace(TINY, n_layers=4, d_model=512, n_heads=8, n_kv_heads=2, head_dim=64, ffn_dim=1024,
+                              vocab=4096, micro_layers=2, stop_mode=STOP_FORCED, dtype=BF16)
+
+
+def _teacher_forced(om, shp, prompts, budgets, steps, sched, seed, debug_steps):
+    orcs = oracle_groups_for(om, prompts, budgets, steps, sched, record=True)
+    teacher = [o.groups for o in orcs]
+    rt = _runtime(shp, seed, prompts.shape[0], prompts.shape[1], steps)
+    res = run_gpu(rt, prompts, budgets, steps, sched, teacher=teacher, debug_steps=debug_steps)
+    tol = TOL[shp.dtype]
+    ties = exact = 0
+    for b, o in enumerate(orcs):
+        decs = {(d.step, d.k): d for d in o.decisions}
+        assert len(res.own[b]) == len(o.groups)
+        for step, toks in enumerate(res.own[b]):
+            assert len(toks) == len(o.groups[step])          # group boundaries exact
+            for k, t in enumerate(toks):
+                lg = res.logits.get((b, step, k))
+                if lg is not None:
+                    d = decs[(step, k)]
+                    assert np.max(np.abs(lg - d.logits)) <= tol, (b, step, k)
+                    assert np.max(np.abs(res.hidden[(b, step, k)] - d.h)) <= tol, (b, step, k)
+                r = check_decision(decs[(step, k)], t, lg, tol)
+                ties += r == "near_tie"
+                exact += r == "exact"
+        st = res.stats[b]
+        assert st["kv_len"] == o.kv_len and st["gen_slots"] == o.gen_slots and st["tokens"] == o.tokens
+        assert st["groups"] == len(o.groups) and st["device_error"] == 0
+    return exact, ties
+
+
+def test_small_bf16_teacher_forced_ragged_batch(torch_cuda):
+    shp = SMALL16
+    B, P, steps = 3, 100, 24
+    prompts = synth.prompt_ids(77, B, P, shp.vocab)
+    sched = synth.group_schedule(78, B, steps + 1, 4)
+    budgets = [0, 17, 40]
+    om = OracleHam(shp, 76)
+    exact, ties = _teacher_forced(om, shp, prompts, budgets, steps, sched, 76, debug_steps=steps + 1)
+    assert ties <= max(1, exact // 50)
+
+
+def test_1b_bf16_teacher_forced_prefix(torch_cuda):
+    # configuration 2 shape and prompt length; the first macro-steps against the oracle
+    w = WORKLOADS["c2_1b_bf16"]
+    shp = w.shape
+    steps = 6
+    prompts = synth.prompt_ids(w.seed_prompt, 1, w.prompt_len, shp.vocab)
+    sched = synth.group_schedule(w.seed_sched, 1, steps + 1, 4)
+    om = OracleHam(shp, w.seed_weights)
+    exact, ties = _teacher_forced(om, shp, prompts, [w.max_new], steps, sched, w.seed_weights,
+                                  debug_steps=steps + 1)
+    assert ties <= 1

@@ -2,11 +2,11 @@
 
 Test infrastructure only (see the package docstring).
 
-Numeric contract (bf16 models): weights are bf16; the operand of every matrix
-product is rounded to bf16 just before the product (``_rnd``); K and V are stored
-rounded to bf16, Q is rounded after RoPE; the residual stream, norms, softmax,
-logits and the stop logit are kept at full precision (here float64).  For fp32
-models ``_rnd`` is the identity and everything is float64.
+Numeric contract (bf16 models): the weights and the KV cache are bf16 (K and V
+are rounded to bf16 when stored, ``_rnd``); every activation, including the
+operands of the matrix products, the residual stream, norms, softmax, logits and
+the stop logit, is kept at full precision (here float64).  For fp32 models
+``_rnd`` is the identity and everything is float64.
 """
 from __future__ import annotations
 
@@ -219,11 +219,11 @@ class OracleHam:
         captured = {}
         X = X.astype(np.float64).copy()
         for li, L in enumerate(layers):
-            u = self._rnd(self.rmsnorm(X, L.g1))
+            u = self.rmsnorm(X, L.g1)
             q = L.wq.matvec(u).reshape(T, H, hd)
             k = L.wk.matvec(u).reshape(T, Hk, hd)
             v = L.wv.matvec(u).reshape(T, Hk, hd)
-            q = self._rnd(self.rope(q, pos))
+            q = self.rope(q, pos)
             k = self._rnd(self.rope(k, pos))
             v = self._rnd(v)
             Kc, Vc = caches[li]
@@ -232,12 +232,12 @@ class OracleHam:
             Vc = np.concatenate([Vc, v.astype(kv_dtype)], axis=0)
             caches[li] = [Kc, Vc]
             o = self.attend(q, Kc, Vc, [S0 + t + 1 for t in range(T)])
-            o = self._rnd(o.reshape(T, H * hd))
+            o = o.reshape(T, H * hd)
             X = X + L.wo.matvec(o)
-            w = self._rnd(self.rmsnorm(X, L.g2))
+            w = self.rmsnorm(X, L.g2)
             g = L.wg.matvec(w)
             up = L.wu.matvec(w)
-            act = self._rnd(g / (1.0 + np.exp(-g)) * up)
+            act = g / (1.0 + np.exp(-g)) * up
             X = X + L.wd.matvec(act)
             if (li + 1) in capture:
                 captured[li + 1] = X.copy()
@@ -252,10 +252,9 @@ class OracleHam:
     def decide(self, x_row: np.ndarray, g: np.ndarray, record: bool):
         """Normed hidden -> (argmax token, stop logit); lowest index wins ties."""
         h = self.rmsnorm(x_row, g)
-        hr = self._rnd(h)
-        logits = self.Wlm.matvec(hr[None, :])[0]
+        logits = self.Wlm.matvec(h[None, :])[0]
         t = int(np.argmax(logits))
-        st = float(self.ws.f64()[0] @ hr)
+        st = float(self.ws.f64()[0] @ h)
         return t, st, h, (logits.astype(np.float32) if record else None)
 
     def embed_group(self, group: Sequence[int]) -> np.ndarray:
@@ -266,18 +265,17 @@ class OracleHam:
         s = self.s
         H, hd = s.n_heads, s.head_dim
         e = self.embed_rows(group) + self.P.f64(0, n)       # learned relative positions 0..n-1
-        qbar = self._rnd(e.mean(axis=0))                     # query = mean of the inputs
-        er = self._rnd(e)
+        qbar = e.mean(axis=0)                                # query = mean of the inputs
         Q = self.Aq.matvec(qbar[None, :])[0].reshape(H, hd)
-        K = self.Ak.matvec(er).reshape(n, H, hd)
-        Vv = self.Av.matvec(er).reshape(n, H, hd)
+        K = self.Ak.matvec(e).reshape(n, H, hd)
+        Vv = self.Av.matvec(e).reshape(n, H, hd)
         o = np.zeros((H, hd))
         for h in range(H):
             sc = K[:, h, :] @ Q[h] / math.sqrt(hd)
             a = np.exp(sc - sc.max())
             a /= a.sum()
             o[h] = a @ Vv[:, h, :]
-        y = self._rnd(self.Ao.matvec(self._rnd(o.reshape(1, H * hd)))[0])
+        y = self.Ao.matvec(o.reshape(1, H * hd))[0]
         return self.Alin.matvec(y[None, :])[0]
 
     # ------------------------------------------------------------------ loop

@@ -58,6 +58,30 @@ template <> struct Frag<float> {
   }
 };
 
+// Activation operands of the matrix products (rows of logical width W).
+// fp32 models keep fp32 rows.  bf16 models keep each fp32 value v as the bf16
+// pair hi = bf16(v), lo = bf16(v - hi) (16 significant bits) in two planes per
+// row, [hi 0..W) [lo 0..W), so that each plane loads as 16-byte fragments; a
+// product then takes two bf16 matrix-core instructions, hi and lo.
+template <typename T> struct Act;
+template <> struct Act<float> {
+  static constexpr bool SPLIT = false;
+  static constexpr int PL = 1;
+  static __device__ __forceinline__ void put(void* base, size_t row, int W, int i, float v) {
+    ((float*)base)[row * W + i] = v;
+  }
+};
+template <> struct Act<bf16> {
+  static constexpr bool SPLIT = true;
+  static constexpr int PL = 2;
+  static __device__ __forceinline__ void put(void* base, size_t row, int W, int i, float v) {
+    bf16* r = (bf16*)base + row * 2 * W;
+    const bf16 h = f2bf(v);
+    r[i] = h;
+    r[W + i] = f2bf(v - bf2f(h));
+  }
+};
+
 __device__ __forceinline__ u4 ld16(const void* p) { return *reinterpret_cast<const u4*>(p); }
 // streamed once per step (weights, KV): non-temporal hint so they do not displace reused lines
 __device__ __forceinline__ u4 ld16_stream(const void* p) {
@@ -73,6 +97,19 @@ __device__ __forceinline__ u4 pack_frag_bf16(const float* v) {
   r.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
   r.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
   return r;
+}
+
+// one product step with an activation fragment pair as the A operand
+template <typename T>
+__device__ __forceinline__ void mma_act(f4& acc, const u4& xhi, const u4& xlo, const u4& w) {
+  Frag<T>::mma(acc, xhi, w);
+  if constexpr (Act<T>::SPLIT) Frag<T>::mma(acc, xlo, w);
+}
+// ... and as the B operand
+template <typename T>
+__device__ __forceinline__ void mma_act_b(f4& acc, const u4& a, const u4& xhi, const u4& xlo) {
+  Frag<T>::mma(acc, a, xhi);
+  if constexpr (Act<T>::SPLIT) Frag<T>::mma(acc, a, xlo);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

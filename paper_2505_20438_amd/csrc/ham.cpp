@@ -139,11 +139,12 @@ Layout make_layout(const ham_config* c) {
   const size_t R = y.rows_max;
   y.x = take((size_t)y.rows_dec * y.d * 4);
   y.xp = take((size_t)y.Tc * y.d * 4);
-  y.xn = take(R * std::max(y.d, y.HD) * es);
+  // activation operands: 4 bytes per value (fp32, or a bf16 hi/lo pair)
+  y.xn = take(R * std::max(y.d, y.HD) * 4);
   y.qkv = take(R * std::max(y.QKV, 3 * y.HD) * 4);
-  y.q = take(R * y.HD * es);
-  y.ao = take(R * y.HD * es);
-  y.act = take(R * y.F * es);
+  y.q = take(R * y.HD * 4);
+  y.ao = take(R * y.HD * 4);
+  y.act = take(R * y.F * 4);
   y.part = take((size_t)MAX_GEMM_SPLIT * 64 * y.Nmax * 4);
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);
@@ -152,9 +153,9 @@ Layout make_layout(const ham_config* c) {
   y.bidx = take((size_t)(y.Vpad / 32) * 64 * 4);
   y.stopb = take(64 * 4);
   y.ctx = take((size_t)y.B * y.C * y.d * 4);
-  y.emb_in = take((size_t)5 * y.B * y.d * es);
-  y.emb_o = take((size_t)y.B * y.HD * es);
-  y.emb_y = take((size_t)y.B * y.d * es);
+  y.emb_in = take((size_t)5 * y.B * y.d * 4);
+  y.emb_o = take((size_t)y.B * y.HD * 4);
+  y.emb_y = take((size_t)y.B * y.d * 4);
   y.loc_layer = al((size_t)y.B * y.Hk * LOCAL_SLOTS * y.hd * es);
   y.Kloc = take(y.loc_layer * y.M);
   y.VTloc = take(y.loc_layer * y.M);

@@ -52,8 +52,8 @@ template <> struct PFrag<float> {
 // `limit_of_row` gives, for this lane's row, the first slot it may not see.
 template <typename T, int HD>
 __device__ __forceinline__ void attn_block(const T* Kb, const T* Vb, int S, int base, int limit,
-                                           const u4* qf, float scale, float& mrun, float& lrun,
-                                           f4* o) {
+                                           const u4* qf, const u4* ql, float scale, float& mrun,
+                                           float& lrun, f4* o) {
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16, TT = KB / 16;
   const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
   float sc[KB / 4];
@@ -63,7 +63,7 @@ __device__ __forceinline__ void attn_block(const T* Kb, const T* Vb, int S, int 
     const T* kp = Kb + (size_t)slot * HD + g * EPL;
     f4 s = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int f = 0; f < NF; ++f) Frag<T>::mma(s, ld16_stream(kp + f * KB), qf[f]);
+    for (int f = 0; f < NF; ++f) mma_act_b<T>(s, ld16_stream(kp + f * KB), qf[f], ql[f]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int sl = base + g * (KB / 4) + 4 * t + i;
@@ -121,16 +121,21 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
   const int s1 = min(nval, s0 + chunk);
   const T* Kb = (const T*)a.K + ri.b * a.sb + kvh * a.sh;
   const T* Vb = (const T*)a.VT + ri.b * a.sb + kvh * a.sh;
-  u4 qf[NF];
-  const T* qp = (const T*)a.q + (size_t)r * a.ldq + (size_t)(kvh * grp + r16) * HD + g * EPL;
+  u4 qf[NF], ql[NF];
+  constexpr int PL = Act<T>::PL;
+  const T* qp = (const T*)a.q + (size_t)r * a.ldq * PL + (size_t)(kvh * grp + r16) * HD + g * EPL;
 #pragma unroll
-  for (int f = 0; f < NF; ++f) qf[f] = (r16 < grp) ? ld16(qp + f * KB) : zero16();
+  for (int f = 0; f < NF; ++f) {
+    qf[f] = (r16 < grp) ? ld16(qp + f * KB) : zero16();
+    ql[f] = (Act<T>::SPLIT && r16 < grp) ? ld16(qp + a.ldq + f * KB) : zero16();
+  }
   f4 o[ND];
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
-  for (int base = s0; base < s1; base += KB) attn_block<T, HD>(Kb, Vb, a.S, base, s1, qf, scale, mrun, lrun, o);
+  for (int base = s0; base < s1; base += KB)
+    attn_block<T, HD>(Kb, Vb, a.S, base, s1, qf, ql, scale, mrun, lrun, o);
 
   if (a.nsplit == 1) {
 #pragma unroll
@@ -138,10 +143,10 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
       const int j = 4 * g + i;
       const float lj = __shfl(lrun, j & 15, WAVE);
       if (j < grp) {
-        T* op = (T*)a.o + (size_t)r * a.ldo + (size_t)(kvh * grp + j) * HD + r16;
+        const int c0 = (kvh * grp + j) * HD + r16;
         const float inv = lj > 0.f ? 1.0f / lj : 0.f;
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) op[dt * 16] = from_f<T>(o[dt][i] * inv);
+        for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, r, a.ldo, c0 + dt * 16, o[dt][i] * inv);
       }
     }
     return;
@@ -167,7 +172,7 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
   for (int j = 0; j < grp; ++j) {
     float M = -INFINITY;
     for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, pb[((size_t)s * grp + j) * rec + HD]);
-    T* op = (T*)a.o + (size_t)r * a.ldo + (size_t)(kvh * grp + j) * HD;
+    const int c0 = (kvh * grp + j) * HD;
     for (int d = lane; d < HD; d += 64) {
       float L = 0.f, O = 0.f;
       if (M != -INFINITY) {
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
           O += wgt * ps[d];
         }
       }
-      op[d] = from_f<T>(L > 0.f ? O / L : 0.f);
+      Act<T>::put(a.o, r, a.ldo, c0 + d, L > 0.f ? O / L : 0.f);
     }
   }
 }
@@ -197,10 +202,14 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
   const T* Vb = (const T*)a.VT + r0.b * a.sb + kvh * a.sh;
   const int qrow = row0 + r16;
   const bool qok = qrow < a.R;
-  u4 qf[NF];
-  const T* qp = (const T*)a.q + (size_t)(qok ? qrow : row0) * a.ldq + (size_t)h * HD + g * EPL;
+  u4 qf[NF], ql[NF];
+  constexpr int PL = Act<T>::PL;
+  const T* qp = (const T*)a.q + (size_t)(qok ? qrow : row0) * a.ldq * PL + (size_t)h * HD + g * EPL;
 #pragma unroll
-  for (int f = 0; f < NF; ++f) qf[f] = qok ? ld16(qp + f * KB) : zero16();
+  for (int f = 0; f < NF; ++f) {
+    qf[f] = qok ? ld16(qp + f * KB) : zero16();
+    ql[f] = (Act<T>::SPLIT && qok) ? ld16(qp + a.ldq + f * KB) : zero16();
+  }
   // causal: row with slot s sees slots [0, s]; rows past the chunk see nothing
   const int limit = qok ? r0.slot + r16 + 1 : 0;
   const int wave_end = r0.slot + min(15, a.R - 1 - row0) + 1;
@@ -211,17 +220,16 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
   const float scale = 1.0f / sqrtf((float)HD);
   for (int base = 0; base < wave_end; base += KB) {
     // per-lane limit: the score mask uses this lane's query row (r16)
-    attn_block<T, HD>(Kb, Vb, a.S, base, limit, qf, scale, mrun, lrun, o);
+    attn_block<T, HD>(Kb, Vb, a.S, base, limit, qf, ql, scale, mrun, lrun, o);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * g + i;  // query row within the wave
     const float lj = __shfl(lrun, j, WAVE);
     if (row0 + j < a.R) {
-      T* op = (T*)a.o + (size_t)(row0 + j) * a.ldo + (size_t)h * HD + r16;
       const float inv = lj > 0.f ? 1.0f / lj : 0.f;
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) op[dt * 16] = from_f<T>(o[dt][i] * inv);
+      for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, row0 + j, a.ldo, h * HD + r16 + dt * 16, o[dt][i] * inv);
     }
   }
 }

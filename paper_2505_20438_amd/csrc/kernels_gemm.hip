@@ -24,9 +24,8 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nb, int r
     o[ne] = ve;
     o[no] = vo;
   } else if constexpr (EPI == EPI_OP) {
-    T* o = (T*)a.out + (size_t)m * a.ldo;
-    o[ne] = from_f<T>(ve);
-    o[no] = from_f<T>(vo);
+    Act<T>::put(a.out, m, a.ldo, ne, ve);
+    Act<T>::put(a.out, m, a.ldo, no, vo);
   } else if constexpr (EPI == EPI_RESID) {
     float* o = (float*)a.out + (size_t)m * a.ldo;
     const float xe = o[ne] + ve, xo = o[no] + vo;
@@ -44,9 +43,8 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nb, int r
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
     // gate rows and up rows are interleaved in blocks of 16: pair (gate, up) of feature f
-    T* o = (T*)a.out + (size_t)m * a.ldo;
     const float sg = ve / (1.0f + expf(-ve));
-    o[nb / 2 + r16] = from_f<T>(sg * vo);
+    Act<T>::put(a.out, m, a.ldo, nb / 2 + r16, sg * vo);
   }
 }
 
@@ -81,13 +79,15 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   const T* wrow[TN];
 #pragma unroll
   for (int j = 0; j < TN; ++j) wrow[j] = W + (size_t)(n0 + 16 * j + r16) * a.K + g * EPL;
+  constexpr int PL = Act<T>::PL;
+  const int lo_off = Act<T>::SPLIT ? a.ldx : 0;  // offset of the lo plane within a row
   const T* xrow[MT];
   bool xok[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
     const int m = 16 * i + r16;
     xok[i] = m < a.M;
-    xrow[i] = X + (size_t)(xok[i] ? m : 0) * a.ldx + g * EPL;
+    xrow[i] = X + (size_t)(xok[i] ? m : 0) * a.ldx * PL + g * EPL;
   }
 
   constexpr int U = 4;
@@ -98,28 +98,34 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int j = 0; j < TN; ++j) bw[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * KB);
-    u4 ax[U][MT];
+    u4 ax[U][MT], axl[U][MT];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int i = 0; i < MT; ++i) ax[u][i] = xok[i] ? ld16(xrow[i] + (size_t)(f + u) * KB) : zero16();
+      for (int i = 0; i < MT; ++i) {
+        ax[u][i] = xok[i] ? ld16(xrow[i] + (size_t)(f + u) * KB) : zero16();
+        axl[u][i] = (Act<T>::SPLIT && xok[i]) ? ld16(xrow[i] + lo_off + (size_t)(f + u) * KB) : zero16();
+      }
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) Frag<T>::mma(acc[i][j], ax[u][i], bw[u][j]);
+        for (int j = 0; j < TN; ++j) mma_act<T>(acc[i][j], ax[u][i], axl[u][i], bw[u][j]);
   }
   for (; f < f1; ++f) {
-    u4 bw[TN], ax[MT];
+    u4 bw[TN], ax[MT], axl[MT];
 #pragma unroll
     for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * KB);
 #pragma unroll
-    for (int i = 0; i < MT; ++i) ax[i] = xok[i] ? ld16(xrow[i] + (size_t)f * KB) : zero16();
+    for (int i = 0; i < MT; ++i) {
+      ax[i] = xok[i] ? ld16(xrow[i] + (size_t)f * KB) : zero16();
+      axl[i] = (Act<T>::SPLIT && xok[i]) ? ld16(xrow[i] + lo_off + (size_t)f * KB) : zero16();
+    }
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) Frag<T>::mma(acc[i][j], ax[i], bw[j]);
+      for (int j = 0; j < TN; ++j) mma_act<T>(acc[i][j], ax[i], axl[i], bw[j]);
   }
 
   // reduce the four waves' k-slices (fixed order: wave 0 + 1 + 2 + 3)
@@ -248,7 +254,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB;
   constexpr int LDR = 5;  // u4 per LDS row: 4 used + 1 pad against bank conflicts
-  __shared__ u4 sA[2][128 * LDR];
+  constexpr int NA = Act<T>::PL;  // activation planes (hi, lo)
+  __shared__ u4 sA[2][NA][128 * LDR];
   __shared__ u4 sB[2][128 * LDR];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -258,20 +265,26 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
   const T* X = (const T*)a.X;
   const int lr = tid >> 1, lc = (tid & 1) * 2;
   const bool aok = m0 + lr < a.M, bok = n0 + lr < a.N;
-  const T* ap = X + (size_t)(aok ? m0 + lr : 0) * a.ldx + lc * EPL;
+  const T* ap = X + (size_t)(aok ? m0 + lr : 0) * a.ldx * NA + lc * EPL;
   const T* bp = W + (size_t)(bok ? n0 + lr : 0) * a.K + lc * EPL;
   const int nst = a.K / KB;
-  u4 ra0, ra1, rb0, rb1;
+  u4 ra[NA][2], rb0, rb1;
   auto gload = [&](int s) {
     const size_t k = (size_t)s * KB;
-    ra0 = aok ? ld16(ap + k) : zero16();
-    ra1 = aok ? ld16(ap + k + EPL) : zero16();
+#pragma unroll
+    for (int p = 0; p < NA; ++p) {
+      ra[p][0] = aok ? ld16(ap + (size_t)p * a.ldx + k) : zero16();
+      ra[p][1] = aok ? ld16(ap + (size_t)p * a.ldx + k + EPL) : zero16();
+    }
     rb0 = bok ? ld16_stream(bp + k) : zero16();
     rb1 = bok ? ld16_stream(bp + k + EPL) : zero16();
   };
   auto sstore = [&](int buf) {
-    sA[buf][lr * LDR + lc] = ra0;
-    sA[buf][lr * LDR + lc + 1] = ra1;
+#pragma unroll
+    for (int p = 0; p < NA; ++p) {
+      sA[buf][p][lr * LDR + lc] = ra[p][0];
+      sA[buf][p][lr * LDR + lc + 1] = ra[p][1];
+    }
     sB[buf][lr * LDR + lc] = rb0;
     sB[buf][lr * LDR + lc + 1] = rb1;
   };
@@ -286,15 +299,18 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
   for (int s = 0; s < nst; ++s) {
     const int cur = s & 1;
     if (s + 1 < nst) gload(s + 1);
-    u4 af[4], bfr[4];
+    u4 af[4], afl[4], bfr[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = sA[cur][(wm * 64 + i * 16 + r16) * LDR + g];
+    for (int i = 0; i < 4; ++i) {
+      af[i] = sA[cur][0][(wm * 64 + i * 16 + r16) * LDR + g];
+      afl[i] = sA[cur][NA - 1][(wm * 64 + i * 16 + r16) * LDR + g];
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) bfr[j] = sB[cur][(wn * 64 + j * 16 + r16) * LDR + g];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) Frag<T>::mma(acc[i][j], af[i], bfr[j]);
+      for (int j = 0; j < 4; ++j) mma_act<T>(acc[i][j], af[i], afl[i], bfr[j]);
     if (s + 1 < nst) sstore(cur ^ 1);
     __syncthreads();
   }

@@ -23,10 +23,9 @@ __global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a) {
   for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
   ss = block_sum256(ss, sh);
   const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
-  T* o = (T*)a.out + (size_t)r * a.ldo;
   for (int i = threadIdx.x; i < a.d; i += 256) {
     const float v = x[i] * inv * a.g[i];
-    o[i] = from_f<T>(v);
+    Act<T>::put(a.out, r, a.ldo, i, v);
     if (a.hid) a.hid[(size_t)r * a.ldh + i] = v;
   }
 }
@@ -60,9 +59,8 @@ __global__ __launch_bounds__(64) void k_rope_append(RopeArgs a) {
       const float c = a.cos_t[(size_t)ri.pos * half + i], sn = a.sin_t[(size_t)ri.pos * half + i];
       const float y1 = x1 * c - x2 * sn, y2 = x2 * c + x1 * sn;
       if (hh < a.H) {
-        T* q = (T*)a.q + (size_t)r * a.ldq + (size_t)hh * a.hd;
-        q[i] = from_f<T>(y1);
-        q[i + half] = from_f<T>(y2);
+        Act<T>::put(a.q, r, a.ldq, hh * a.hd + i, y1);
+        Act<T>::put(a.q, r, a.ldq, hh * a.hd + i + half, y2);
       } else if (ri.enabled) {
         T* k = (T*)a.K + ri.b * a.sb + (hh - a.H) * a.sh + (size_t)ri.slot * a.hd;
         k[i] = from_f<T>(y1);
@@ -110,7 +108,6 @@ __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
     for (int i = threadIdx.x; i < d; i += 256) a.x[(size_t)b * a.ldx + i] = to_f<T>(E[(size_t)tok[0] * d + i]);
   } else if (on && n > 1) {
     // e_j = E[t_j] + P[j]; query = mean_j e_j; rows of the embedder's projection GEMM
-    T* rows = (T*)a.emb_in + (size_t)b * 5 * d;
     for (int i = threadIdx.x; i < d; i += 256) {
       float sum = 0.f;
       for (int j = 0; j < 4; ++j) {
@@ -119,9 +116,9 @@ __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
           e = to_f<T>(E[(size_t)tok[j] * d + i]) + to_f<T>(P[(size_t)j * d + i]);
           sum += e;
         }
-        rows[(size_t)(1 + j) * d + i] = from_f<T>(e);
+        Act<T>::put(a.emb_in, (size_t)b * 5 + 1 + j, d, i, e);
       }
-      rows[i] = from_f<T>(sum / (float)n);
+      Act<T>::put(a.emb_in, (size_t)b * 5, d, i, sum / (float)n);
     }
   }
   __syncthreads();
@@ -176,11 +173,10 @@ __global__ __launch_bounds__(64) void k_embed_attn(EmbedAttnArgs a) {
     e[j] = j < n ? expf(w[j] - m) : 0.f;
     sum += e[j];
   }
-  T* o = (T*)a.out + (size_t)b * HD + (size_t)h * hd;
   for (int i = threadIdx.x; i < hd; i += 64) {
     float acc = 0.f;
     for (int j = 0; j < n; ++j) acc += e[j] * base[(size_t)(1 + j) * 3 * HD + 2 * HD + (size_t)h * hd + i];
-    o[i] = from_f<T>(acc / sum);
+    Act<T>::put(a.out, b, HD, h * hd + i, acc / sum);
   }
 }
 

@@ -123,6 +123,5 @@ def oracle_groups_for(om, prompts, budgets, steps, sched=None, record=False):
     out = []
     for b in range(prompts.shape[0]):
         forced = (lambda st, b=b: int(sched[b, st])) if sched is not None else None
-        out.append(om.generate(prompts[b], int(budgets[b]), 0 if budgets[b] else steps, forced=forced,
-                               record=record))
+        out.append(om.generate(prompts[b], int(budgets[b]), steps, forced=forced, record=record))
     return out

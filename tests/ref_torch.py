@@ -3,8 +3,8 @@
 Written separately from ``oracle/`` on purpose: torch library primitives
 (``scaled_dot_product_attention``, ``multi_head_attention_forward``, complex
 rotation for RoPE) and *full recomputation* of every forward instead of KV
-caches.  Float64 throughout, with the bf16 rounding points applied through
-torch's own bfloat16 conversion.  Slow (quadratic); tiny shapes only.
+caches.  Float64 throughout; in bf16 models only the stored K and V are rounded,
+through torch's own bfloat16 conversion.  Slow (quadratic); tiny shapes only.
 """
 from __future__ import annotations
 
@@ -71,23 +71,23 @@ class RefHam:
         H, Hk, hd = s.n_heads, s.n_kv_heads, s.head_dim
         outs = []
         for L in layers:
-            u = self.rnd(self.norm(X))
-            q = self.rnd(self.rope((u @ L["q"].T).view(T, H, hd), pos))
+            u = self.norm(X)
+            q = self.rope((u @ L["q"].T).view(T, H, hd), pos)
             k = self.rnd(self.rope((u @ L["k"].T).view(T, Hk, hd), pos))
             v = self.rnd((u @ L["v"].T).view(T, Hk, hd))
             rep = H // Hk
             kk = k.repeat_interleave(rep, dim=1).transpose(0, 1)
             vv = v.repeat_interleave(rep, dim=1).transpose(0, 1)
             o = F.scaled_dot_product_attention(q.transpose(0, 1), kk, vv, is_causal=True)
-            o = self.rnd(o.transpose(0, 1).reshape(T, H * hd))
+            o = o.transpose(0, 1).reshape(T, H * hd)
             X = X + o @ L["o"].T
-            w = self.rnd(self.norm(X))
-            X = X + self.rnd(F.silu(w @ L["g"].T) * (w @ L["u"].T)) @ L["dn"].T
+            w = self.norm(X)
+            X = X + (F.silu(w @ L["g"].T) * (w @ L["u"].T)) @ L["dn"].T
             outs.append(X)
         return outs
 
     def decide(self, x):
-        h = self.rnd(self.norm(x))
+        h = self.norm(x)
         logits = self.Wlm @ h
         return int(torch.argmax(logits)), float(self.ws @ h), logits
 
@@ -97,15 +97,15 @@ class RefHam:
         s = self.s
         n = len(group)
         e = self.E[list(group)] + self.P[:n]
-        qbar = self.rnd(e.mean(0))
+        qbar = e.mean(0)
         o, _ = F.multi_head_attention_forward(
-            qbar.view(1, 1, -1), self.rnd(e).view(n, 1, -1), self.rnd(e).view(n, 1, -1),
+            qbar.view(1, 1, -1), e.view(n, 1, -1), e.view(n, 1, -1),
             s.d_model, s.n_heads, None, None, None, None, False, 0.0,
             torch.eye(s.d_model, dtype=torch.float64), None, training=False, need_weights=False,
             use_separate_proj_weight=True, q_proj_weight=self.Aq, k_proj_weight=self.Ak,
             v_proj_weight=self.Av)
         # the identity out-projection above leaves the concatenated heads; A_o then A_lin follow
-        return self.Alin @ self.rnd(self.Ao @ self.rnd(o.view(-1)))
+        return self.Alin @ (self.Ao @ o.view(-1))
 
     def generate(self, prompt, budget, macro_steps, forced=None, record=None):
         """Groups per step; ``record`` (a list) receives (token, stop logit, logits) per decision."""

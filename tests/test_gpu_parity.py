@@ -102,6 +102,19 @@ def _teacher_forced(om, shp, prompts, budgets, steps, sched, seed, debug_steps):
     res = run_gpu(rt, prompts, budgets, steps, sched, teacher=teacher, debug_steps=debug_steps)
     tol = TOL[shp.dtype]
     ties = exact = 0
+    errs = []
+    for b, o in enumerate(orcs):
+        decs = {(d.step, d.k): d for d in o.decisions}
+        for (bb, step, k), lg in res.logits.items():
+            if bb == b:
+                d = decs[(step, k)]
+                errs.append((float(np.max(np.abs(lg - d.logits))), float(np.max(np.abs(res.hidden[(b, step, k)] - d.h))),
+                             float(np.sqrt(np.mean((res.hidden[(b, step, k)] - d.h) ** 2))), b, step, k))
+    e = np.array([x[:3] for x in errs])
+    print("decisions", len(errs), "logit err max/mean", e[:, 0].max(), e[:, 0].mean(),
+          "hidden max/mean", e[:, 1].max(), e[:, 1].mean(), "hidden rms mean", e[:, 2].mean())
+    for x in sorted(errs, key=lambda x: -x[1])[:8]:
+        print("  worst", x)
     for b, o in enumerate(orcs):
         decs = {(d.step, d.k): d for d in o.decisions}
         assert len(res.own[b]) == len(o.groups)
@@ -133,11 +146,22 @@ def test_small_bf16_teacher_forced_ragged_batch(torch_cuda):
     assert ties <= max(1, exact // 50)
 
 
+def test_small_fp32_teacher_forced_ragged_batch(torch_cuda):
+    # the same shape in fp32: any error beyond rounding would show up here
+    shp = dataclasses.replace(SMALL16, dtype=0)
+    B, P, steps = 3, 100, 24
+    prompts = synth.prompt_ids(77, B, P, shp.vocab)
+    sched = synth.group_schedule(78, B, steps + 1, 4)
+    om = OracleHam(shp, 76)
+    exact, ties = _teacher_forced(om, shp, prompts, [0, 17, 40], steps, sched, 76, debug_steps=steps + 1)
+    assert ties == 0
+
+
 def test_1b_bf16_teacher_forced_prefix(torch_cuda):
     # configuration 2 shape and prompt length; the first macro-steps against the oracle
     w = WORKLOADS["c2_1b_bf16"]
     shp = w.shape
-    steps = 6
+    steps = 4
     prompts = synth.prompt_ids(w.seed_prompt, 1, w.prompt_len, shp.vocab)
     sched = synth.group_schedule(w.seed_sched, 1, steps + 1, 4)
     om = OracleHam(shp, w.seed_weights)

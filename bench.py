@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""Benchmark of the HAMburger macro-step decode loop on one MI355X.
+
+One step = one whole generation of the workload: prefill (timed separately and
+excluded from the decode rate) then macro-steps until every sequence has spent
+its output-token budget.  Inputs (weights, prompts, group-length schedule) are
+seeded and resident in HBM before timing starts.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2_1b_bf16]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+from synth.configs import BF16, WORKLOADS, Workload  # noqa: E402
+
+METRIC = "output tokens/s at 1 GPU; KV entries per output token; decode HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+PROF_NAMES = ["qkv", "o_proj", "gate_up", "down", "micro_gemm", "embed_gemm", "lm_head_k0", "lm_head_micro",
+              "attn_decode"]
+DOMINANT_KERNEL = {
+    2: "k_gemm_skinny<bf16, 2, 1, EPI_SWIGLU, 0> (base-layer gate/up weight streaming, SwiGLU epilogue)",
+}
+
+
+def group_lengths(sched: np.ndarray, budget: int) -> list:
+    """Realised group sizes of one sequence: the forced length, cut by the budget."""
+    out, emitted, s = [], 0, 0
+    while emitted < budget:
+        n = min(int(sched[s]), budget - emitted)
+        out.append(n)
+        emitted += n
+        s += 1
+    return out
+
+
+def algorithmic_bytes(w: Workload, lens: list) -> float:
+    """Bytes the decode loop must move (closed form over the realised schedule).
+
+    Per macro-step s (consuming group s-1, emitting group s), while any sequence
+    runs: all base-layer weights and the LM head once; the embedder weights if a
+    consumed group has more than one token; for every micro step some sequence
+    still needs, the micro-decoder weights and the LM head again; per running
+    sequence the K and V of every visible slot, plus the new slot written.
+    """
+    s = w.shape
+    es = 2 if s.dtype == BF16 else 4
+    d, H, Hk, hd, F, V = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim, s.ffn_dim, s.vocab
+    layer = (2 * d * H * hd + 2 * d * Hk * hd + 3 * d * F) * es
+    W_base, W_micro = s.n_layers * layer, s.micro_layers * layer
+    W_lm = (V + 1) * d * es
+    W_emb = 5 * d * d * es
+    kv_slot = s.n_layers * 2 * Hk * hd * es
+    steps = max(len(l) for l in lens) - 1
+    total = 0.0
+    for st in range(1, steps + 1):
+        run = [b for b in range(len(lens)) if st < len(lens[b])]
+        if not run:
+            break
+        total += W_base + W_lm
+        if any(lens[b][st - 1] > 1 for b in run):
+            total += W_emb
+        micro = max(lens[b][st] for b in run) - 1
+        total += micro * (W_micro + W_lm)
+        for b in run:
+            kv_len = w.prompt_len + st
+            total += kv_len * kv_slot + kv_slot
+    return total
+
+
+def cpu_baseline(w: Workload, sample_steps: int) -> dict:
+    """The float64 oracle on this host's cores over the first macro-steps of one sequence."""
+    from oracle import OracleHam
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    om = OracleHam(w.shape, w.seed_weights)
+    prompt = synth.prompt_ids(w.seed_prompt, 1, w.prompt_len, w.shape.vocab)[0]
+    sched = synth.group_schedule(w.seed_sched, 1, sample_steps + 2, w.shape.max_group)[0]
+    timing = {}
+    res = om.generate(prompt, w.max_new, sample_steps, forced=lambda st: int(sched[st]), timing=timing)
+    tokens = res.tokens - len(res.groups[0])   # tokens emitted by the timed macro-steps
+    return {"value": tokens / timing["decode_s"], "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{w.name}: sequence 0, prompt {w.prompt_len}, first {sample_steps} macro-steps "
+                      f"({tokens} tokens, {timing['decode_s']:.1f} s of decode; prefill {timing['prefill_s']:.1f} s "
+                      f"excluded), float64 numpy, {platform.processor() or platform.machine()}"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="c2_1b_bf16", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-steps", type=int, default=3, help="macro-steps of the oracle sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); the batch would shard "
+              "data-parallel over sequences with no exchange, which is not built.", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2505_20438_amd import ham
+
+    w = WORKLOADS[args.workload]
+    s = w.shape
+    if w.max_new <= 0:
+        raise SystemExit("the benchmark needs a budgeted workload")
+    B, P = w.batch, w.prompt_len
+    dev = torch.device("cuda:0")
+    cfg = ham.make_config(n_layers=s.n_layers, d_model=s.d_model, n_heads=s.n_heads, n_kv_heads=s.n_kv_heads,
+                          head_dim=s.head_dim, ffn_dim=s.ffn_dim, vocab=s.vocab, micro_layers=s.micro_layers,
+                          max_group=s.max_group, stop_mode=s.stop_mode, stop_id=s.stop_id, dtype=s.dtype,
+                          max_batch=B, max_prompt=P, max_steps=w.max_new)
+    rt = ham.HamRuntime(cfg, w.seed_weights, "cuda:0")
+    stream = rt.stream
+    prompts = torch.from_numpy(synth.prompt_ids(w.seed_prompt, B, P, s.vocab)).to(dev)
+    sched_np = synth.group_schedule(w.seed_sched, B, w.max_new + 1, s.max_group)
+    sched = torch.from_numpy(np.ascontiguousarray(sched_np.T)).to(dev)   # [step][B], resident
+    budgets = [w.max_new] * B
+    lens = [group_lengths(sched_np[b], w.max_new) for b in range(B)]
+    n_steps = max(len(l) for l in lens) - 1
+    tokens_per_run = sum(budgets)
+
+    def one_run(profile: bool = False):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record(stream)
+        rt.prefill(prompts, budgets, sched[0])
+        e1.record(stream)
+        if profile:
+            ham.load_library().ham_profile(rt.handle, 1)
+        for st in range(1, n_steps + 1):
+            rt.macro_step(sched[st])
+        e2.record(stream)
+        if profile:
+            ham.load_library().ham_profile(rt.handle, 0)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1), e1.elapsed_time(e2)
+
+    for _ in range(args.warmup):
+        one_run()
+    stats = rt.kv_stats()
+    torch.cuda.synchronize()
+    decode_ms, prefill_ms = [], []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        pf, dc = one_run()
+        prefill_ms.append(pf)
+        decode_ms.append(dc)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stats = rt.kv_stats()
+    assert all(st["tokens"] == w.max_new and st["device_error"] == 0 for st in stats), stats
+    gen_slots = sum(st["gen_slots"] for st in stats)
+    dec_ms = float(np.mean(decode_ms))
+    value = tokens_per_run / (dec_ms / 1000.0)
+    alg_bytes = algorithmic_bytes(w, lens)
+
+    # per-kernel-class timing: one more run with HIP events around every launch of
+    # the classes (same launch configuration, outside the timed runs above)
+    one_run(profile=True)
+    prof = (ham.HamProfT * ham.HAM_PROF_KINDS)()
+    ham.check(ham.load_library().ham_profile_read(rt.handle, prof, ham.HAM_PROF_KINDS))
+    kernels = {}
+    for i, name in enumerate(PROF_NAMES):
+        p = prof[i]
+        if p.launches:
+            kernels[name] = {"launches": p.launches, "avg_us": 1000.0 * p.ms / p.launches,
+                             "bytes_per_launch": p.bytes / p.launches,
+                             "gbs": (p.bytes / 1e9) / (p.ms / 1000.0) if p.ms > 0 else None}
+    dom = max(("qkv", "o_proj", "gate_up", "down", "lm_head_k0", "attn_decode"),
+              key=lambda k: kernels.get(k, {}).get("avg_us", 0) * kernels.get(k, {}).get("launches", 0))
+    kd = kernels[dom]
+    roofline = {"bound": "hbm", "achieved": kd["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": kd["gbs"] / HBM_PEAK_GBS, "traffic": None, "kernel": dom,
+                "bytes_per_launch": kd["bytes_per_launch"], "avg_us": kd["avg_us"]}
+    if dom == "gate_up" and s.dtype == BF16 and B <= 16:
+        roofline["kernel_name"] = DOMINANT_KERNEL[2]
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": dec_ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if s.dtype == BF16 else "f32", "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "prompt_len": P, "output_tokens_per_seq": w.max_new,
+                   "layers": s.n_layers, "d_model": s.d_model, "micro_layers": s.micro_layers,
+                   "schedule": "forced geometric group lengths p=1/2, cap 4", "macro_steps": n_steps},
+        "kv_entries_per_output_token": gen_slots / float(sum(st["tokens"] for st in stats)),
+        "decode_hbm_gbs": (alg_bytes / 1e9) / (dec_ms / 1000.0),
+        "decode_hbm_frac": (alg_bytes / 1e9) / (dec_ms / 1000.0) / HBM_PEAK_GBS,
+        "algorithmic_bytes_per_run": alg_bytes,
+        "prefill_ms": float(np.mean(prefill_ms)),
+        "us_per_macro_step": 1000.0 * dec_ms / n_steps,
+        "wall_s_timed": wall,
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    if args.cpu_steps > 0:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_steps)
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -66,7 +66,7 @@ typedef struct ham_config {
   float norm_eps;       /* RMSNorm epsilon, e.g. 1e-5 */
   int32_t dtype;        /* HAM_F32 or HAM_BF16 (weights, KV, GEMM operands) */
   /* capacity, fixed for the life of the model */
-  int32_t max_batch;    /* sequences per call, 1..1024 */
+  int32_t max_batch;    /* sequences per call, 1..64 */
   int32_t max_prompt;   /* longest prompt */
   int32_t max_steps;    /* macro-steps after prefill (one KV slot per sequence each) */
 } ham_config;
@@ -156,6 +156,40 @@ int ham_steps_done(const ham_model* m);
  * (*interleave = 1: gate rows at 32*(r/16) + r%16, up rows 16 later). */
 int ham_tensor_info(const ham_config* cfg, int32_t tensor_id, size_t* offset, int32_t* rows,
                     int32_t* cols, int32_t* interleave);
+
+/* Per-kernel-class timing of later calls (diagnostics for the benchmark).
+ * While enabled, every launch of the classes below is bracketed by a pair of
+ * HIP events on the model's stream and its algorithmic bytes are recorded
+ * (weight GEMMs: weights + fp32 activation rows in + fp32 results out;
+ * attention: K and V of every visible slot).  Base-layer and k = 0 launches
+ * always do their work; micro-step and embedder launches may exit at once when
+ * no sequence needs them, so their bytes are upper bounds.
+ *   HAM_PROF_QKV, _O, _GU, _DOWN   base-layer projections (decode)
+ *   HAM_PROF_MICRO                 micro-decoder layer GEMMs
+ *   HAM_PROF_EMBED                 compositional-embedder GEMMs
+ *   HAM_PROF_HEAD0                 LM head + argmax + stop test, k = 0
+ *   HAM_PROF_HEADK                 the same for micro steps k >= 1
+ *   HAM_PROF_ATTN                  split-K decode attention, base layers
+ * ham_profile(m, 1) clears the records and starts; ham_profile(m, 0) stops.
+ * ham_profile_read synchronises the stream and fills out[kind] for
+ * kind < n (launches, summed event time in ms, summed bytes). */
+#define HAM_PROF_QKV 0
+#define HAM_PROF_O 1
+#define HAM_PROF_GU 2
+#define HAM_PROF_DOWN 3
+#define HAM_PROF_MICRO 4
+#define HAM_PROF_EMBED 5
+#define HAM_PROF_HEAD0 6
+#define HAM_PROF_HEADK 7
+#define HAM_PROF_ATTN 8
+#define HAM_PROF_KINDS 9
+typedef struct ham_prof_t {
+  int32_t launches;
+  double ms;
+  double bytes;
+} ham_prof_t;
+int ham_profile(ham_model* m, int enable);
+int ham_profile_read(ham_model* m, ham_prof_t* out, int n);
 
 const char* ham_last_error(void);
 void ham_destroy(ham_model* m);

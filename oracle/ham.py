@@ -12,6 +12,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import time
 from typing import Callable, List, Optional, Sequence
 
 import numpy as np
@@ -319,13 +320,16 @@ class OracleHam:
 
     def generate(self, prompt: Sequence[int], budget: int, macro_steps: int,
                  forced: Optional[Callable[[int], int]] = None, record: bool = False,
-                 inputs: Optional[List[np.ndarray]] = None) -> SeqResult:
+                 inputs: Optional[List[np.ndarray]] = None, timing: Optional[dict] = None) -> SeqResult:
         """Prefill then ``macro_steps`` macro-steps (or until the budget is spent).
 
         ``forced(step)`` gives the forced group length (FORCED stop mode).
         If ``inputs`` is a list, the base-model input vectors and their positions
-        are appended to it (for the prefill-versus-incremental check).
+        are appended to it (for the prefill-versus-incremental check).  If
+        ``timing`` is a dict it receives the wall time of prefill and of the
+        macro-steps (``prefill_s``, ``decode_s``).
         """
+        t_start = time.perf_counter()
         s = self.s
         forced = forced or (lambda step: s.max_group)
         P = len(prompt)
@@ -346,6 +350,7 @@ class OracleHam:
         emitted = len(group)
         pos_last = P - 1
         step = 0
+        t_prefill = time.perf_counter()
         while True:
             if budget > 0 and emitted >= budget:
                 break
@@ -366,6 +371,9 @@ class OracleHam:
                                     record, decisions)
             groups.append(group)
             emitted += len(group)
+        if timing is not None:
+            timing["prefill_s"] = t_prefill - t_start
+            timing["decode_s"] = time.perf_counter() - t_prefill
         self.last_caches = caches
         kv_len = caches[0][0].shape[0]
         return SeqResult(groups=groups, kv_len=kv_len, prompt_slots=P, gen_slots=kv_len - P,

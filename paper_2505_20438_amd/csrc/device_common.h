@@ -133,27 +133,6 @@ __device__ __forceinline__ float block_sum256(float v, float* sh4) {
   return (sh4[0] + sh4[1]) + (sh4[2] + sh4[3]);
 }
 
-// Last-arriver handshake: every workgroup publishes its partial results, then
-// bumps `counter`; the one that sees `expected - 1` owns the final reduction and
-// resets the counter for the next launch.  No workgroup ever waits on another.
-// Every wave releases its own stores at agent scope first (the L2 of one XCD is
-// not coherent with the others for ordinary device memory); the owner acquires
-// before it reads what the others wrote.
-__device__ __forceinline__ bool last_arriver(int* counter, int expected, int* sh_flag) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    int last = (prev == expected - 1);
-    if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *sh_flag = last;
-  }
-  __syncthreads();
-  const bool last = *sh_flag != 0;
-  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return last;
-}
-
 // any nonzero among n flags (n small); used to skip work no sequence needs
 __device__ __forceinline__ bool any_flag(const int* flags, int n) {
   if (flags == nullptr) return true;

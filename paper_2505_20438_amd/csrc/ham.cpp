@@ -173,9 +173,44 @@ struct ham_model {
   char* ws;
   hipStream_t s;
   SeqPtrs sp;
-  int batch = 0, prompt_len = 0, steps_done = -1, has_teacher = 0;
+  int batch = 0, prompt_len = 0, steps_done = -1, has_teacher = 0, kv_visible = 0;
   float tau;
   float* dbg = nullptr;
+  // optional per-class event timing
+  struct Rec { int kind; hipEvent_t a, b; double bytes; };
+  bool prof_on = false;
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t pool_used = 0;
+  hipEvent_t ev() {
+    if (pool_used == pool.size()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      pool.push_back(e);
+    }
+    return pool[pool_used++];
+  }
+  int prof_kind = -1;
+  double prof_bytes = 0;
+  hipEvent_t prof_a = nullptr;
+  void pbegin(int kind, double bytes) {
+    if (!prof_on) return;
+    prof_kind = kind;
+    prof_bytes = bytes;
+    prof_a = ev();
+    if (prof_a) hipEventRecord(prof_a, s);
+  }
+  void pend() {
+    if (!prof_on || !prof_a) return;
+    hipEvent_t b = ev();
+    if (!b) return;
+    hipEventRecord(b, s);
+    recs.push_back(Rec{prof_kind, prof_a, b, prof_bytes});
+    prof_a = nullptr;
+  }
+  ~ham_model() {
+    for (hipEvent_t e : pool) hipEventDestroy(e);
+  }
   // typed views
   template <typename P> P* W(size_t off) const { return (P*)(w + off); }
   template <typename P> P* WS(size_t off) const { return (P*)(ws + off); }
@@ -198,26 +233,65 @@ SeqPtrs seq_ptrs(char* st, const Layout& y) {
 
 int dtype_of(const ham_model* m) { return m->cfg.dtype; }
 
-// one transformer layer (base layer j < L, micro layer j >= L) over R rows
+// algorithmic bytes of one weight GEMM: weights once, activation rows in (4 B per
+// value), fp32 results out
+double gemm_bytes(const Layout& y, int N, int K, int M) {
+  return (double)N * K * y.es + (double)M * K * 4 + (double)M * N * 4;
+}
+
+// A split-K GEMM result still held as partials (the next RMSNorm adds it to x).
+struct Pending {
+  const float* part = nullptr;
+  int nsplit = 0, M = 0;
+};
+
+int gemm_p(ham_model* m, int epi, const GemmArgs& a, int max_split, int kind, int* nsplit) {
+  m->pbegin(kind, gemm_bytes(m->y, a.N, a.K, a.M));
+  const bool base = kind >= HAM_PROF_QKV && kind <= HAM_PROF_DOWN;
+  const int rc = launch_gemm(dtype_of(m), epi, a, max_split, m->s, base ? 0 : 1, nsplit);
+  m->pend();
+  return rc;
+}
+
+// RMSNorm of R rows of x (row r reads x row r*stride + off) into the operand buffer,
+// after adding a pending split-K result to those rows and copying them to ctx
+void norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* g, Pending& pend, float* ctx,
+               int ldctx, float* hid, const int* gate, int gate_n) {
+  const Layout& y = m->y;
+  NormArgs na{};
+  na.x = x; na.ldx = y.d; na.row_stride = stride; na.row_off = off; na.g = g; na.d = y.d; na.R = R;
+  na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d; na.hid = hid; na.ldh = y.d;
+  na.part = pend.part; na.nsplit = pend.nsplit; na.pM = pend.M; na.ctx = ctx; na.ldctx = ldctx;
+  na.gate = gate; na.gate_n = gate_n;
+  launch_rmsnorm(dtype_of(m), na, m->s);
+  pend = Pending{};
+}
+
+// one transformer layer (base layer j < L, micro layer j >= L) over R rows.
+// On entry `pend` may hold the previous layer's down-projection partials (folded
+// into x by the first norm, which also copies the updated rows to ctx_prev); on
+// exit it holds this layer's, if split.
 int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefill, void* Kc, void* VTc,
-              long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, float* ctx_out,
-              int ldctx) {
+              long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
+              float* ctx_prev, int ldctx, int kv_visible) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
-  NormArgs na{};
-  na.x = x; na.ldx = y.d; na.row_stride = 1; na.row_off = 0; na.g = m->W<float>(y.g1[j]); na.d = y.d; na.R = R;
-  na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d; na.gate = gate; na.gate_n = gate_n;
-  launch_rmsnorm(dt, na, s);
+  const bool base = !prefill && j < y.L;
+  const auto gk = [&](int kind) { return prefill ? -1 : (base ? kind : HAM_PROF_MICRO); };
+  const int split = prefill ? 1 : MAX_GEMM_SPLIT;
+  int ns = 1;
+  norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
 
   GemmArgs ga{};
-  ga.part = m->WS<float>(y.part); ga.counters = m->WS<int>(y.gctr); ga.gate = gate; ga.gate_n = gate_n;
+  ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n;
   ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = R;
   ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
-  if (launch_gemm(dt, EPI_F32, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "qkv gemm shape");
+  if (gemm_p(m, EPI_F32, ga, split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
 
   RopeArgs ra{};
   ra.qkv = m->WS<float>(y.qkv); ra.ldqkv = y.QKV; ra.R = R; ra.q = m->WS<char>(y.q); ra.ldq = y.HD;
+  ra.part = ns > 1 ? m->WS<float>(y.part) : nullptr; ra.nsplit = ns;
   ra.K = Kc; ra.VT = VTc; ra.sb = sb; ra.sh = sh; ra.S = S; ra.H = y.H; ra.Hkv = y.Hk; ra.hd = y.hd;
   ra.cos_t = m->W<float>(y.cos_t); ra.sin_t = m->W<float>(y.sin_t); ra.max_pos = y.max_pos; ra.rm = rm;
   ra.gate = gate; ra.gate_n = gate_n;
@@ -226,61 +300,64 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefi
   AttnArgs aa{};
   aa.q = m->WS<char>(y.q); aa.ldq = y.HD; aa.K = Kc; aa.VT = VTc; aa.sb = sb; aa.sh = sh; aa.S = S;
   aa.H = y.H; aa.Hkv = y.Hk; aa.hd = y.hd; aa.R = R; aa.nsplit = attn_split; aa.o = m->WS<char>(y.ao);
-  aa.ldo = y.HD; aa.part = m->WS<float>(y.apart); aa.counters = m->WS<int>(y.actr); aa.rm = rm;
+  aa.ldo = y.HD; aa.part = m->WS<float>(y.apart); aa.rm = rm;
   aa.gate = gate; aa.gate_n = gate_n;
-  if ((prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s)) != 0)
-    return fail(HAM_EINVAL, "attention shape");
+  m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
+  const int arc = prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s);
+  m->pend();
+  if (arc != 0) return fail(HAM_EINVAL, "attention shape");
 
   ga.W = m->W<char>(y.Wo[j]); ga.N = y.d; ga.K = y.HD; ga.X = m->WS<char>(y.ao); ga.ldx = y.HD;
   ga.out = x; ga.ldo = y.d;
-  if (launch_gemm(dt, EPI_RESID, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "o-proj gemm shape");
+  if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_O), &ns)) return fail(HAM_EINVAL, "o-proj gemm shape");
+  if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
 
-  na.g = m->W<float>(y.g2[j]);
-  launch_rmsnorm(dt, na, s);
+  norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n);
 
   ga.W = m->W<char>(y.Wgu[j]); ga.N = 2 * y.F; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
   ga.out = m->WS<char>(y.act); ga.ldo = y.F;
-  if (launch_gemm(dt, EPI_SWIGLU, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "gate/up gemm shape");
+  if (gemm_p(m, EPI_SWIGLU, ga, 1, gk(HAM_PROF_GU), &ns)) return fail(HAM_EINVAL, "gate/up gemm shape");
 
   ga.W = m->W<char>(y.Wd[j]); ga.N = y.d; ga.K = y.F; ga.X = m->WS<char>(y.act); ga.ldx = y.F;
-  ga.out = x; ga.ldo = y.d; ga.ctx = ctx_out; ga.ldctx = ldctx;
-  if (launch_gemm(dt, EPI_RESID, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "down gemm shape");
+  ga.out = x; ga.ldo = y.d;
+  if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_DOWN), &ns)) return fail(HAM_EINVAL, "down gemm shape");
+  if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
   return HAM_OK;
 }
 
-// final norm of one row per sequence + LM head argmax + stop head + stop test (decision k)
-int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, const float* g,
-                 int* out_tokens, int* out_lens) {
+// final norm of one row per sequence (folding in pending partials, capturing the
+// last context row) + LM head with per-tile argmax and stop logit, then the
+// decision and stop test (decision k)
+int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, const float* g, Pending& pend,
+                 float* ctx_last, int* out_tokens, int* out_lens) {
   const Layout& y = m->y;
-  const int dt = dtype_of(m);
   const int B = m->batch;
-  NormArgs na{};
-  na.x = x; na.ldx = y.d; na.row_stride = row_stride; na.row_off = row_off; na.g = g; na.d = y.d; na.R = B;
-  na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d;
-  na.hid = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + ((size_t)k * y.B) * y.d : nullptr; na.ldh = y.d;
-  na.gate = m->sp.active; na.gate_n = B;
-  launch_rmsnorm(dt, na, m->s);
+  float* hid = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + ((size_t)k * y.B) * y.d : nullptr;
+  norm_rows(m, x, B, row_stride, row_off, g, pend, ctx_last, y.C * y.d, hid, m->sp.active, B);
 
   GemmArgs ga{};
   ga.W = m->W<char>(y.Wlm); ga.N = y.Vpad; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = B;
-  ga.counters = m->WS<int>(y.gctr); ga.gate = m->sp.active; ga.gate_n = B;
+  ga.gate = m->sp.active; ga.gate_n = B;
   DecideArgs& d = ga.dec;
   d.st = m->sp; d.B = B; d.k = k; d.mode = m->cfg.stop_mode; d.stop_id = m->cfg.stop_id; d.G = y.G; d.V = y.V;
   d.tau = m->tau; d.out_tokens = out_tokens; d.out_lens = out_lens; d.has_teacher = m->has_teacher;
   d.dbg_logits = m->dbg ? m->dbg + (size_t)k * y.B * y.V : nullptr;
   d.dbg_stop = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + (size_t)4 * y.B * y.d + (size_t)k * y.B : nullptr;
   d.stop_buf = m->WS<float>(y.stopb); d.best_val = m->WS<float>(y.bval); d.best_idx = m->WS<int>(y.bidx);
-  if (launch_gemm(dt, EPI_ARGMAX, ga, 1, m->s)) return fail(HAM_EINVAL, "lm head shape");
+  int ns = 1;
+  if (gemm_p(m, EPI_ARGMAX, ga, 1, k == 0 ? HAM_PROF_HEAD0 : HAM_PROF_HEADK, &ns))
+    return fail(HAM_EINVAL, "lm head shape");
+  launch_decide(d, y.Vpad / 32, B, m->s);
   return HAM_OK;
 }
 
 // decision k = 0 from the base model, then the micro steps (all gated on device)
-int decode_tail(ham_model* m, int* out_tokens, int* out_lens) {
+int decode_tail(ham_model* m, Pending& pend, float* ctx_last, int* out_tokens, int* out_lens) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   const int B = m->batch;
   float* x = m->WS<float>(y.x);
-  int rc = run_decision(m, 0, x, 1, 0, m->W<float>(y.gf), out_tokens, out_lens);
+  int rc = run_decision(m, 0, x, 1, 0, m->W<float>(y.gf), pend, ctx_last, out_tokens, out_lens);
   if (rc) return rc;
   const long long lsb = (long long)y.Hk * LOCAL_SLOTS * y.hd, lsh = (long long)LOCAL_SLOTS * y.hd;
   for (int k = 1; k < y.G; ++k) {
@@ -291,14 +368,15 @@ int decode_tail(ham_model* m, int* out_tokens, int* out_lens) {
     RowMap rm{};
     rm.mode = k == 1 ? ROWS_MICRO1 : ROWS_MICROK; rm.C = y.C; rm.k = k; rm.st = m->sp;
     const int R = k == 1 ? B * (y.C + 1) : B;
+    Pending mp_pend;
     for (int mj = 0; mj < y.M; ++mj) {
       rc = run_layer(m, y.L + mj, R, rm, x, false, m->WS<char>(y.Kloc + mj * y.loc_layer),
-                     m->WS<char>(y.VTloc + mj * y.loc_layer), lsb, lsh, LOCAL_SLOTS, 1, m->sp.active, B,
-                     nullptr, 0);
+                     m->WS<char>(y.VTloc + mj * y.loc_layer), lsb, lsh, LOCAL_SLOTS, 1, m->sp.active, B, mp_pend,
+                     nullptr, 0, k == 1 ? B * (y.C + 1) * (y.C + 2) / 2 : B * (y.C + k));
       if (rc) return rc;
     }
-    rc = run_decision(m, k, x, k == 1 ? y.C + 1 : 1, k == 1 ? y.C : 0, m->W<float>(y.gmf), out_tokens,
-                      out_lens);
+    rc = run_decision(m, k, x, k == 1 ? y.C + 1 : 1, k == 1 ? y.C : 0, m->W<float>(y.gmf), mp_pend, nullptr,
+                      out_tokens, out_lens);
     if (rc) return rc;
   }
   return HAM_OK;
@@ -475,8 +553,9 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
       RowMap rm{};
       rm.mode = ROWS_PREFILL; rm.b = b; rm.t0 = t0; rm.st = m->sp;
       for (int l = 0; l < y.L; ++l) {
+        Pending none;
         int rc = run_layer(m, l, R, rm, xp, true, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer,
-                           sb, sh, y.S, 1, nullptr, 0, nullptr, 0);
+                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0);
         if (rc) return rc;
         if (last)
           for (int c = 0; c < y.C; ++c)
@@ -486,7 +565,8 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
       if (last) launch_copy_row(xp + (size_t)(R - 1) * y.d, x + (size_t)b * y.d, y.d, s);
     }
   }
-  int rc = decode_tail(m, d_out_tokens, d_out_lens);
+  Pending none;
+  int rc = decode_tail(m, none, nullptr, d_out_tokens, d_out_lens);
   if (rc) return rc;
   HIP_TRY(hipGetLastError());
   m->steps_done = 0;
@@ -515,20 +595,30 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
 
   // compositional embedder (Sec. 3.2), skipped on device unless some group has > 1 token
   GemmArgs ga{};
-  ga.part = m->WS<float>(y.part); ga.counters = m->WS<int>(y.gctr); ga.gate = m->sp.fused; ga.gate_n = B;
+  ga.part = m->WS<float>(y.part); ga.gate = m->sp.fused; ga.gate_n = B;
   ga.W = m->W<char>(y.Aqkv); ga.N = 3 * y.HD; ga.K = y.d; ga.X = m->WS<char>(y.emb_in); ga.ldx = y.d;
   ga.M = 5 * B; ga.out = m->WS<float>(y.qkv); ga.ldo = 3 * y.HD;
-  if (launch_gemm(dt, EPI_F32, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "embedder gemm shape");
+  int ns = 1;
+  if (gemm_p(m, EPI_F32, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
   EmbedAttnArgs ea{};
   ea.proj = m->WS<float>(y.qkv); ea.fused = m->sp.fused; ea.B = B; ea.H = y.H; ea.d = y.d; ea.hd = y.hd;
+  ea.part = ns > 1 ? m->WS<float>(y.part) : nullptr; ea.nsplit = ns;
   ea.out = m->WS<char>(y.emb_o);
   launch_embed_attn(dt, ea, s);
   ga.W = m->W<char>(y.Ao); ga.N = y.d; ga.K = y.HD; ga.X = m->WS<char>(y.emb_o); ga.ldx = y.HD; ga.M = B;
   ga.out = m->WS<char>(y.emb_y); ga.ldo = y.d;
-  if (launch_gemm(dt, EPI_OP, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "embedder gemm shape");
+  if (gemm_p(m, EPI_OP, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
+  if (ns > 1) {
+    ga.nsplit = ns;
+    launch_split_reduce(dt, EPI_OP, ga, s);
+  }
   ga.W = m->W<char>(y.Alin); ga.N = y.d; ga.K = y.d; ga.X = m->WS<char>(y.emb_y); ga.ldx = y.d;
   ga.out = x; ga.ldo = y.d; ga.rowmask = m->sp.fused;
-  if (launch_gemm(dt, EPI_XMASK, ga, MAX_GEMM_SPLIT, s)) return fail(HAM_EINVAL, "embedder gemm shape");
+  if (gemm_p(m, EPI_XMASK, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
+  if (ns > 1) {
+    ga.nsplit = ns;
+    launch_split_reduce(dt, EPI_XMASK, ga, s);
+  }
 
   // base forward: one new KV slot per running sequence
   RowMap rm{};
@@ -536,16 +626,19 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
   const int kv_max = m->prompt_len + m->steps_done + 1;
   const int nsplit = attn_splits(m, B, kv_max);
+  m->kv_visible = B * kv_max;  // every running sequence holds the same count at this step (upper bound)
   float* ctx = m->WS<float>(y.ctx);
+  Pending pend;
+  float* ctx_prev = nullptr;  // context slot of the previous layer's output, captured by the next norm
   for (int l = 0; l < y.L; ++l) {
-    float* co = nullptr;
-    for (int c = 0; c < y.C; ++c)
-      if (y.ctx_l[c] == l + 1) co = ctx + (size_t)c * y.d;
     int rc = run_layer(m, l, B, rm, x, false, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer, sb,
-                       sh, y.S, nsplit, m->sp.step_on, B, co, y.C * y.d);
+                       sh, y.S, nsplit, m->sp.step_on, B, pend, ctx_prev, y.C * y.d, m->kv_visible);
     if (rc) return rc;
+    ctx_prev = nullptr;
+    for (int c = 0; c < y.C; ++c)
+      if (y.ctx_l[c] == l + 1) ctx_prev = ctx + (size_t)c * y.d;
   }
-  int rc = decode_tail(m, d_out_tokens, d_out_lens);
+  int rc = decode_tail(m, pend, ctx_prev, d_out_tokens, d_out_lens);
   if (rc) return rc;
   HIP_TRY(hipGetLastError());
   m->steps_done += 1;
@@ -587,6 +680,31 @@ int ham_set_debug(ham_model* m, void* d_buf, size_t bytes) {
 }
 
 int ham_steps_done(const ham_model* m) { return m ? m->steps_done : -1; }
+
+int ham_profile(ham_model* m, int enable) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  if (enable) {
+    m->recs.clear();
+    m->pool_used = 0;
+  }
+  m->prof_on = enable != 0;
+  return HAM_OK;
+}
+
+int ham_profile_read(ham_model* m, ham_prof_t* out, int n) {
+  if (!m || !out || n < 0) return fail(HAM_EINVAL, "bad arguments");
+  HIP_TRY(hipStreamSynchronize(m->s));
+  for (int k = 0; k < n; ++k) out[k] = ham_prof_t{0, 0.0, 0.0};
+  for (const auto& r : m->recs) {
+    if (r.kind < 0 || r.kind >= n) continue;
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, r.a, r.b));
+    out[r.kind].launches += 1;
+    out[r.kind].ms += ms;
+    out[r.kind].bytes += r.bytes;
+  }
+  return HAM_OK;
+}
 
 void ham_destroy(ham_model* m) { delete m; }
 

@@ -54,7 +54,6 @@ struct DecideArgs {
   float* stop_buf;   // [B] stop logits (workspace)
   float* best_val;   // [n_wg][B] argmax partials
   int* best_idx;
-  int* any_active;   // unused placeholder for future fusion
 };
 
 struct GemmArgs {
@@ -64,7 +63,7 @@ struct GemmArgs {
   float* ctx; int ldctx;           // RESID: copy of updated rows (optional)
   const int* rowmask;              // XMASK: rows to store
   const int* gate; int gate_n;     // launch does nothing unless a gate flag is set
-  float* part; int* counters; int nsplit;  // split-K partials / last-arriver counters
+  float* part; int* counters; int nsplit;  // split-K partials [nsplit][M][N] (written when nsplit > 1)
   DecideArgs dec;                  // ARGMAX only
 };
 
@@ -76,19 +75,24 @@ struct AttnArgs {
   int S;                           // slot capacity (row length of VT)
   int H, Hkv, hd, R, nsplit;
   void* o; int ldo;                // o [R][H*hd] (storage type)
-  float* part; int* counters;      // split partials [R][Hkv][nsplit][grp][hd+2]
+  float* part; int* counters;      // split partials [R][Hkv][nsplit][grp][hd+2]  (counters unused)
   RowMap rm;
   const int* gate; int gate_n;
 };
 
 // ---------------------------------------------------------------- launchers
 typedef hipStream_t Stream;
-int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s);
+// tag 0: base-layer launch (distinct kernel name in profiles), 1: any other.
+// *nsplit receives the k-split used; above 1 the result is fp32 partials in a.part.
+int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, int tag, int* nsplit);
+int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s);
+int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s);
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s);
 int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s);
 
 struct RopeArgs {
   const float* qkv; int ldqkv, R;  // [R][(H+2Hkv)hd] fp32 projections
+  const float* part; int nsplit;   // or split-K partials [nsplit][R][ldqkv] to sum
   void* q; int ldq;                // out q [R][H*hd]
   void* K; void* VT; long long sb, sh; int S;
   int H, Hkv, hd;
@@ -100,7 +104,9 @@ struct RopeArgs {
 int launch_rope_append(int dtype, const RopeArgs& a, Stream s);
 
 struct NormArgs {
-  const float* x; int ldx; int row_stride, row_off;  // input row r = x[(r*row_stride+row_off)*ldx]
+  float* x; int ldx; int row_stride, row_off;        // input row r = x[(r*row_stride+row_off)*ldx]
+  const float* part; int nsplit, pM;                 // pending split-K partials [nsplit][pM][ldx] added to x first
+  float* ctx; int ldctx;                             // optional copy of the updated x rows
   const float* g; int d, R; float eps;
   void* out; int ldo;                                 // storage-type output
   float* hid; int ldh;                                // optional fp32 copy of the normed rows

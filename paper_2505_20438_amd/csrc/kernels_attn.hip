@@ -10,9 +10,9 @@
 // l >> 4), so no data moves between the two products.
 //
 // k_attn_decode: one wave per (query row, kv head, slot split).  The rows of
-//   the matrix products are the q-heads sharing the kv head (GQA).  Splits are
-//   combined with the log-sum-exp rule by the last wave to finish, in a fixed
-//   order.  Used for base decode (ragged kv_len per sequence) and the micro
+//   the matrix products are the q-heads sharing the kv head (GQA).  Splits
+//   write (max, sum, unnormalised output) and k_attn_combine merges them with
+//   the log-sum-exp rule in split order.  Used for base decode (ragged kv_len per sequence) and the micro
 //   decoder's local cache.
 // k_attn_prefill: four waves of 16 consecutive query rows of one head, causal.
 //
@@ -109,7 +109,6 @@ template <typename T, int HD>
 __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16;
-  __shared__ int sh_flag;
   const int lane = threadIdx.x, r16 = lane & 15, g = lane >> 4;
   const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
   const int grp = a.H / a.Hkv;
@@ -168,24 +167,30 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
     pj[HD] = mrun;
     pj[HD + 1] = lrun;
   }
-  if (!last_arriver(a.counters + r * a.Hkv + kvh, a.nsplit, &sh_flag)) return;
-  for (int j = 0; j < grp; ++j) {
-    float M = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, pb[((size_t)s * grp + j) * rec + HD]);
-    const int c0 = (kvh * grp + j) * HD;
-    for (int d = lane; d < HD; d += 64) {
-      float L = 0.f, O = 0.f;
-      if (M != -INFINITY) {
-        for (int s = 0; s < a.nsplit; ++s) {
-          const float* ps = pb + ((size_t)s * grp + j) * rec;
-          const float ms = ps[HD];
-          const float wgt = ms == -INFINITY ? 0.f : __expf(ms - M);
-          L += wgt * ps[HD + 1];
-          O += wgt * ps[d];
-        }
+}
+
+// Log-sum-exp combine of the splits of one (row, head), in split order.
+template <typename T>
+__global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int grp = a.H / a.Hkv, kvh = h / grp, j = h % grp, HD = a.hd;
+  const size_t rec = HD + 2;
+  const float* pb = a.part + (((size_t)r * a.Hkv + kvh) * a.nsplit) * grp * rec;
+  float M = -INFINITY;
+  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, pb[((size_t)s * grp + j) * rec + HD]);
+  for (int d = lane; d < HD; d += 64) {
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
+      for (int s = 0; s < a.nsplit; ++s) {
+        const float* ps = pb + ((size_t)s * grp + j) * rec;
+        const float ms = ps[HD];
+        const float wgt = ms == -INFINITY ? 0.f : __expf(ms - M);
+        L += wgt * ps[HD + 1];
+        O += wgt * ps[d];
       }
-      Act<T>::put(a.o, r, a.ldo, c0 + d, L > 0.f ? O / L : 0.f);
     }
+    Act<T>::put(a.o, r, a.ldo, h * HD + d, L > 0.f ? O / L : 0.f);
   }
 }
 
@@ -240,6 +245,7 @@ static int decode_t(const AttnArgs& a, Stream s) {
   if (a.hd == 64) hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64), 0, s, a);
   else if (a.hd == 128) hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64), 0, s, a);
   else return -1;
+  if (a.nsplit > 1) hipLaunchKernelGGL((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, a);
   return 0;
 }
 template <typename T>

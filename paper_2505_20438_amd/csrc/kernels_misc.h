@@ -16,7 +16,8 @@ struct MacroArgs {
 };
 
 struct EmbedAttnArgs {
-  const float* proj;                // [B*5][3d]
+  const float* proj;                // [B*5][3*H*hd]
+  const float* part; int nsplit;    // or split-K partials [nsplit][B*5][3*H*hd]
   const int* fused;                 // [B] group size when fused, else 0
   int B, H, d, hd;
   void* out;                        // [B][H*hd] storage type

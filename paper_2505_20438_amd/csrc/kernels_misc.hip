@@ -13,14 +13,27 @@ namespace ham {
 
 // ---------------------------------------------------------------- RMSNorm
 // out[r] = g * x / sqrt(mean(x^2) + eps), rounded to the storage type (the GEMM operand)
+// A pending split-K result of the previous GEMM (partials) is first added to the
+// residual row in split order, and the updated row optionally copied out.
 template <typename T>
 __global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   __shared__ float sh[4];
   const int r = blockIdx.x;
-  const float* x = a.x + (size_t)(r * a.row_stride + a.row_off) * a.ldx;
+  const int xr = r * a.row_stride + a.row_off;
+  float* x = a.x + (size_t)xr * a.ldx;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < a.d; i += 256) ss += x[i] * x[i];
+  for (int i = threadIdx.x; i < a.d; i += 256) {
+    float v = x[i];
+    if (a.part) {
+      float p = 0.f;
+      for (int s = 0; s < a.nsplit; ++s) p += a.part[((size_t)s * a.pM + xr) * a.ldx + i];
+      v += p;
+      x[i] = v;
+    }
+    if (a.ctx) a.ctx[(size_t)r * a.ldctx + i] = v;
+    ss += v * v;
+  }
   ss = block_sum256(ss, sh);
   const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
   for (int i = threadIdx.x; i < a.d; i += 256) {
@@ -54,7 +67,19 @@ __global__ __launch_bounds__(64) void k_rope_append(RopeArgs a) {
     return;
   }
   for (int i = threadIdx.x; i < half; i += 64) {
-    const float x1 = src[i], x2 = src[i + half];
+    float x1, x2;
+    if (a.part) {  // sum the split-K partials of the projection in split order
+      x1 = x2 = 0.f;
+      const size_t col = (size_t)hh * a.hd + i;
+      for (int s = 0; s < a.nsplit; ++s) {
+        const float* ps = a.part + ((size_t)s * a.R + r) * a.ldqkv + col;
+        x1 += ps[0];
+        x2 += ps[half];
+      }
+    } else {
+      x1 = src[i];
+      x2 = src[i + half];
+    }
     if (hh < a.H + a.Hkv) {
       const float c = a.cos_t[(size_t)ri.pos * half + i], sn = a.sin_t[(size_t)ri.pos * half + i];
       const float y1 = x1 * c - x2 * sn, y2 = x2 * c + x1 * sn;
@@ -152,16 +177,24 @@ __global__ __launch_bounds__(64) void k_embed_attn(EmbedAttnArgs a) {
   const int n = a.fused[b];
   if (n < 2) return;
   const int hd = a.hd, HD = a.H * a.hd;  // proj row: Q | K | V blocks of H*hd each
-  const float* base = a.proj + (size_t)b * 5 * 3 * HD;
-  const float* Q = base + (size_t)h * hd;
+  // projection value (row, col), summing split-K partials when present
+  auto P = [&](int row, int col) {
+    const size_t idx = ((size_t)b * 5 + row) * 3 * HD + col;
+    if (!a.part) return a.proj[idx];
+    float v = 0.f;
+    for (int s = 0; s < a.nsplit; ++s) v += a.part[(size_t)s * a.B * 5 * 3 * HD + idx];
+    return v;
+  };
   __shared__ float w[4];
+  __shared__ float qs[128];
+  for (int i = threadIdx.x; i < hd; i += 64) qs[i] = P(0, h * hd + i);
+  __syncthreads();
   if (threadIdx.x < 4) {
     const int j = threadIdx.x;
     float s = -INFINITY;
     if (j < n) {
-      const float* K = base + (size_t)(1 + j) * 3 * HD + HD + (size_t)h * hd;
       s = 0.f;
-      for (int i = 0; i < hd; ++i) s += Q[i] * K[i];
+      for (int i = 0; i < hd; ++i) s += qs[i] * P(1 + j, HD + h * hd + i);
       s *= 1.0f / sqrtf((float)hd);
     }
     w[j] = s;
@@ -175,7 +208,7 @@ __global__ __launch_bounds__(64) void k_embed_attn(EmbedAttnArgs a) {
   }
   for (int i = threadIdx.x; i < hd; i += 64) {
     float acc = 0.f;
-    for (int j = 0; j < n; ++j) acc += e[j] * base[(size_t)(1 + j) * 3 * HD + 2 * HD + (size_t)h * hd + i];
+    for (int j = 0; j < n; ++j) acc += e[j] * P(1 + j, 2 * HD + h * hd + i);
     Act<T>::put(a.out, b, HD, h * hd + i, acc / sum);
   }
 }

@@ -17,9 +17,11 @@ HAM_OK, HAM_EINVAL, HAM_ENOMEM, HAM_EHIP, HAM_ESTATE, HAM_ECAP = 0, -1, -2, -3, 
 HAM_F32, HAM_BF16 = 0, 1
 HAM_STOP_HEAD, HAM_STOP_TOKEN, HAM_STOP_FORCED = 0, 1, 2
 
+HAM_PROF_KINDS = 9
+
 EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
             "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
-            "ham_tensor_info", "ham_last_error", "ham_destroy")
+            "ham_tensor_info", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy")
 
 
 class HamConfig(ctypes.Structure):
@@ -40,6 +42,10 @@ class HamKvStats(ctypes.Structure):
         d = {n: getattr(self, n) for n, _ in self._fields_ if n != "len_hist"}
         d["len_hist"] = list(self.len_hist)
         return d
+
+
+class HamProfT(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int32), ("ms", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
 class HamError(RuntimeError):
@@ -72,19 +78,24 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_steps_done.argtypes = [P]
     lib.ham_tensor_info.argtypes = [cfgp, I32, ctypes.POINTER(SZ), ctypes.POINTER(I32), ctypes.POINTER(I32),
                                     ctypes.POINTER(I32)]
+    lib.ham_profile.argtypes = [P, I32]
+    lib.ham_profile_read.argtypes = [P, ctypes.POINTER(HamProfT), I32]
     lib.ham_last_error.restype = ctypes.c_char_p
     lib.ham_destroy.argtypes = [P]
     lib.ham_destroy.restype = None
     for n in ("ham_init_weights", "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug",
-              "ham_steps_done", "ham_tensor_info"):
+              "ham_steps_done", "ham_tensor_info", "ham_profile", "ham_profile_read"):
         getattr(lib, n).restype = I32
     _lib = lib
     return lib
 
 
-def _check(rc: int) -> None:
+def check(rc: int) -> None:
     if rc != HAM_OK:
         raise HamError(rc, load_library().ham_last_error().decode())
+
+
+_check = check
 
 
 def make_config(**kw) -> HamConfig:

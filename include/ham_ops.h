@@ -1,0 +1,49 @@
+/*
+ * libham single-kernel entry points, for parity tests and diagnostics.
+ *
+ * They run the same kernels as ham_macro_step on caller-provided buffers, so a
+ * test can check one step of the decode loop at shapes where running the whole
+ * model through a CPU reference is too slow (e.g. attention over a 32K-slot
+ * cache).  Same conventions as include/ham.h: C functions, HAM_OK or a negative
+ * HAM_E* code, ham_last_error() for the message, "d_" = device pointers, work
+ * enqueued on `hip_stream` and valid after it is synchronised.
+ *
+ * Activation layout ("act rows") of width W: fp32 models store fp32 [W] per row;
+ * bf16 models store each value v as the bf16 pair hi = bf16(v), lo = bf16(v - hi)
+ * in two planes per row, [hi 0..W) [lo 0..W) (4 bytes per value either way).
+ */
+#ifndef HAM_OPS_H
+#define HAM_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Workspace bytes that ham_op_decode_attention needs for `rows` query rows. */
+size_t ham_op_attention_workspace_bytes(int32_t rows, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim);
+
+/* GQA decode attention of one query row per sequence over that sequence's
+ * cache (the base-layer attention of a macro-step over the smashed KV cache,
+ * Sec. 3.1): out[r, h] = softmax_j(q[r, h] . K[r, h/(H/Hkv), j] / sqrt(hd)) V[...]
+ * over slots j < kv_len[r]; rows with enable[r] == 0 (or kv_len 0) get zeros.
+ *  dtype        HAM_F32 or HAM_BF16 (cache element type)
+ *  d_q          act rows [rows][n_heads*head_dim], RoPE already applied
+ *  d_k          [rows][n_kv_heads][slots_cap][head_dim]   (slot-major)
+ *  d_vt         [rows][n_kv_heads][head_dim][slots_cap]   (d-major)
+ *  d_kv_len     int32 [rows], each <= slots_cap; d_enable int32 [rows]
+ *  kv_max       host upper bound of kv_len (chooses the slot split)
+ *  d_out        act rows [rows][n_heads*head_dim]
+ * head_dim 64 or 128, n_heads/n_kv_heads in 1..4, slots_cap a multiple of 64.
+ * HAM_EINVAL on a bad shape, HAM_ENOMEM if the workspace is too small. */
+int ham_op_decode_attention(int32_t dtype, int32_t rows, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                            int32_t slots_cap, const void* d_q, const void* d_k, const void* d_vt,
+                            const int32_t* d_kv_len, const int32_t* d_enable, int32_t kv_max, void* d_out,
+                            void* d_workspace, size_t workspace_bytes, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HAM_OPS_H */

@@ -37,6 +37,27 @@ def _bits_to_f64(u: np.ndarray) -> np.ndarray:
     return (u.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
 
 
+def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray, n_valid: Sequence[int], n_kv_heads: int) -> np.ndarray:
+    """GQA softmax attention: q [T][H][hd]; K, V [S][Hkv][hd]; row t sees slots < n_valid[t];
+    q-head h reads kv-head h // (H / Hkv); scores scaled by 1/sqrt(hd)."""
+    T, H, hd = q.shape
+    kv_of = np.arange(H) // (H // n_kv_heads)
+    out = np.zeros((T, H, hd))
+    scale = 1.0 / math.sqrt(hd)
+    for t in range(T):
+        n = int(n_valid[t])
+        if n == 0:
+            continue
+        Kh = K[:n][:, kv_of, :].astype(np.float64)    # [n][H][hd]
+        Vh = V[:n][:, kv_of, :].astype(np.float64)
+        sc = np.einsum("hd,nhd->hn", q[t], Kh) * scale
+        sc = sc - sc.max(axis=1, keepdims=True)
+        a = np.exp(sc)
+        a /= a.sum(axis=1, keepdims=True)
+        out[t] = np.einsum("hn,nhd->hd", a, Vh)
+    return out
+
+
 # ----------------------------------------------------------------------------
 # weights
 # ----------------------------------------------------------------------------
@@ -189,21 +210,7 @@ class OracleHam:
 
     def attend(self, q: np.ndarray, K: np.ndarray, V: np.ndarray, n_valid: Sequence[int]) -> np.ndarray:
         """Softmax attention: q [T][H][hd]; K, V [S][Hkv][hd]; row t sees slots < n_valid[t]."""
-        s = self.s
-        T, H, hd = q.shape
-        kv_of = np.arange(H) // (H // s.n_kv_heads)     # q-head h reads kv-head h // (H / Hkv)
-        out = np.zeros((T, H, hd))
-        scale = 1.0 / math.sqrt(hd)
-        for t in range(T):
-            n = int(n_valid[t])
-            Kh = K[:n][:, kv_of, :].astype(np.float64)    # [n][H][hd]
-            Vh = V[:n][:, kv_of, :].astype(np.float64)
-            sc = np.einsum("hd,nhd->hn", q[t], Kh) * scale
-            sc = sc - sc.max(axis=1, keepdims=True)
-            a = np.exp(sc)
-            a /= a.sum(axis=1, keepdims=True)
-            out[t] = np.einsum("hn,nhd->hd", a, Vh)
-        return out
+        return attend(q, K, V, n_valid, self.s.n_kv_heads)
 
     def forward_rows(self, layers: Sequence[_Layer], X: np.ndarray, pos: np.ndarray,
                      caches: list, capture: Sequence[int] = ()):

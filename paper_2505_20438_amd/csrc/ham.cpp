@@ -2,6 +2,7 @@
 // sequences of prefill and of one macro-step.  Every arithmetic step runs in
 // the HIP kernels; this file only sequences them on the caller's stream.
 #include "../../include/ham.h"
+#include "../../include/ham_ops.h"
 
 #include <hip/hip_runtime.h>
 
@@ -52,6 +53,8 @@ constexpr int MAX_GEMM_SPLIT = 16;
 constexpr int MAX_ATTN_SPLIT = 64;
 constexpr int LOCAL_SLOTS = 64;
 
+size_t attn_part_bytes(int R, int H, int Hk, int hd);
+
 struct Layout {
   // dims
   int L, M, d, H, Hk, hd, F, V, G, B, P, steps;
@@ -73,8 +76,9 @@ const char* check_cfg(const ham_config* c) {
       c->vocab < 2 || c->micro_layers < 1)
     return "dimensions must be positive (micro_layers >= 1)";
   if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
-  if (c->n_heads % c->n_kv_heads != 0 || c->n_heads / c->n_kv_heads > 16) return "n_heads must be a multiple (<= 16x) of n_kv_heads";
+  if (c->n_heads % c->n_kv_heads != 0 || c->n_heads / c->n_kv_heads > 4) return "n_heads must be a multiple (<= 4x) of n_kv_heads";
   if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32 || c->ffn_dim % 32) return "d_model, n_heads*head_dim and ffn_dim must be multiples of 32";
+  if (c->d_model > 8192) return "d_model must be <= 8192";
   if (c->max_group < 1 || c->max_group > 4) return "max_group must be in 1..4";
   if (c->stop_mode < 0 || c->stop_mode > 2) return "unknown stop_mode";
   if (c->stop_mode == HAM_STOP_TOKEN && (c->stop_id < 0 || c->stop_id >= c->vocab)) return "stop_id out of range";
@@ -148,7 +152,7 @@ Layout make_layout(const ham_config* c) {
   y.part = take((size_t)MAX_GEMM_SPLIT * 64 * y.Nmax * 4);
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);
-  y.apart = take((size_t)y.rows_dec * y.Hk * MAX_ATTN_SPLIT * (y.H / y.Hk) * (y.hd + 2) * 4);
+  y.apart = take(attn_part_bytes(y.rows_dec, y.H, y.Hk, y.hd));
   y.bval = take((size_t)(y.Vpad / 32) * 64 * 4);
   y.bidx = take((size_t)(y.Vpad / 32) * 64 * 4);
   y.stopb = take(64 * 4);
@@ -382,11 +386,21 @@ int decode_tail(ham_model* m, Pending& pend, float* ctx_last, int* out_tokens, i
   return HAM_OK;
 }
 
-int attn_splits(const ham_model* m, int R, int kv_max) {
-  const int kb = m->cfg.dtype == HAM_BF16 ? 32 : 16;
-  int want = (2048 + R * m->y.Hk - 1) / (R * m->y.Hk);
-  const int most = std::max(1, (kv_max + 2 * kb - 1) / (2 * kb));
+// slot splits across workgroups: none while every wave of a workgroup gets at
+// most a few key blocks; otherwise enough to give about 4096 waves in total
+int attn_splits_for(int dtype, int R, int Hk, int kv_max) {
+  const int kb = dtype == HAM_BF16 ? 32 : 16;
+  const int blocks = (kv_max + kb - 1) / kb;
+  if (blocks <= 8 * 8) return 1;  // 8 waves x at most 8 blocks each
+  const int wgs = R * Hk;
+  int want = (4096 / 8 + wgs - 1) / wgs;
+  const int most = std::max(1, blocks / (8 * 2));  // at least 2 blocks per wave
   return std::max(1, std::min(std::min(want, most), MAX_ATTN_SPLIT));
+}
+int attn_splits(const ham_model* m, int R, int kv_max) { return attn_splits_for(m->cfg.dtype, R, m->y.Hk, kv_max); }
+
+size_t attn_part_bytes(int R, int H, int Hk, int hd) {
+  return (size_t)R * Hk * MAX_ATTN_SPLIT * (H / Hk) * (hd + 2) * 4;
 }
 
 }  // namespace
@@ -707,5 +721,36 @@ int ham_profile_read(ham_model* m, ham_prof_t* out, int n) {
 }
 
 void ham_destroy(ham_model* m) { delete m; }
+
+size_t ham_op_attention_workspace_bytes(int32_t rows, int32_t H, int32_t Hk, int32_t hd) {
+  if (rows < 1 || H < 1 || Hk < 1 || H % Hk) return 0;
+  return al(attn_part_bytes(rows, H, Hk, hd));
+}
+
+int ham_op_decode_attention(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, int32_t hd, int32_t S,
+                            const void* d_q, const void* d_k, const void* d_vt, const int32_t* d_kv_len,
+                            const int32_t* d_enable, int32_t kv_max, void* d_out, void* d_ws, size_t ws_bytes,
+                            void* stream) {
+  if (dtype != HAM_F32 && dtype != HAM_BF16) return fail(HAM_EINVAL, "bad dtype");
+  if (rows < 1 || H < 1 || Hk < 1 || H % Hk || H / Hk > 4 || (hd != 64 && hd != 128) || S < 64 || S % 64)
+    return fail(HAM_EINVAL, "bad attention shape");
+  if (kv_max < 0 || kv_max > S) return fail(HAM_EINVAL, "kv_max out of range");
+  if (!d_q || !d_k || !d_vt || !d_kv_len || !d_enable || !d_out || !d_ws) return fail(HAM_EINVAL, "null pointer");
+  if (ws_bytes < attn_part_bytes(rows, H, Hk, hd)) return fail(HAM_ENOMEM, "workspace too small");
+  SeqPtrs sp{};
+  sp.kv_len = const_cast<int*>(d_kv_len);
+  sp.step_on = const_cast<int*>(d_enable);
+  sp.cur_slot = sp.kv_len;  // read by the row map, unused by attention
+  sp.cur_pos = sp.kv_len;
+  AttnArgs aa{};
+  aa.q = d_q; aa.ldq = H * hd; aa.K = d_k; aa.VT = d_vt; aa.sb = (long long)Hk * S * hd;
+  aa.sh = (long long)S * hd; aa.S = S; aa.H = H; aa.Hkv = Hk; aa.hd = hd; aa.R = rows;
+  aa.nsplit = attn_splits_for(dtype, rows, Hk, std::max(kv_max, 1));
+  aa.o = d_out; aa.ldo = H * hd; aa.part = (float*)d_ws;
+  aa.rm.mode = ROWS_DECODE; aa.rm.st = sp;
+  if (launch_attn_decode(dtype, aa, (hipStream_t)stream)) return fail(HAM_EINVAL, "attention shape");
+  HIP_TRY(hipGetLastError());
+  return HAM_OK;
+}
 
 }  // extern "C"

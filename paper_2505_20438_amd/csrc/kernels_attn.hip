@@ -9,8 +9,9 @@
 // l holds the probabilities of row l & 15 for the slot slice of lane group
 // l >> 4), so no data moves between the two products.
 //
-// k_attn_decode: one wave per (query row, kv head, slot split).  The rows of
-//   the matrix products are the q-heads sharing the kv head (GQA).  Splits
+// k_attn_decode: one workgroup per (query row, kv head, slot split), its waves
+//   sharing the slot range.  The rows of the matrix products are the q-heads
+//   sharing the kv head (GQA).  Waves merge in LDS; splits (long contexts only)
 //   write (max, sum, unnormalised output) and k_attn_combine merges them with
 //   the log-sum-exp rule in split order.  Used for base decode (ragged kv_len per sequence) and the micro
 //   decoder's local cache.
@@ -47,23 +48,48 @@ template <> struct PFrag<float> {
   static constexpr bool TWO = false;
 };
 
-// One key block of KB slots starting at `base`: scores for the 16 operand rows
-// (lane: row r16, slots base + g*KB/4 + e), online-softmax update of (m, l, o).
-// `limit_of_row` gives, for this lane's row, the first slot it may not see.
+// The K and V fragments of one key block of KB slots, loaded together (V does
+// not depend on the scores, so both streams are in flight at once).
 template <typename T, int HD>
-__device__ __forceinline__ void attn_block(const T* Kb, const T* Vb, int S, int base, int limit,
-                                           const u4* qf, const u4* ql, float scale, float& mrun,
-                                           float& lrun, f4* o) {
-  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16, TT = KB / 16;
+struct KVBlock {
+  static constexpr int KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16, TT = KB / 16;
+  u4 k[TT][NF];
+  u4 v[ND];
+};
+
+template <typename T, int HD>
+__device__ __forceinline__ void kv_load(KVBlock<T, HD>& blk, const T* Kb, const T* Vb, int S, int base) {
+  using B = KVBlock<T, HD>;
+  constexpr int EPL = Frag<T>::EPL, KB = B::KB;
   const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < B::TT; ++t) {
+    // operand row r16 of tile t holds the slot whose score lane group r16/4 needs
+    const int slot = base + (r16 >> 2) * (KB / 4) + 4 * t + (r16 & 3);
+    const T* kp = Kb + (size_t)slot * HD + g * EPL;
+#pragma unroll
+    for (int f = 0; f < B::NF; ++f) blk.k[t][f] = ld16_stream(kp + f * KB);
+  }
+  const T* vp = Vb + (size_t)r16 * S + base + g * (KB / 4);
+#pragma unroll
+  for (int dt = 0; dt < B::ND; ++dt) blk.v[dt] = ld16_stream(vp + (size_t)dt * 16 * S);
+}
+
+// Scores of the 16 operand rows against the block (lane: row r16, slots
+// base + g*KB/4 + e), masked at `limit`, then the online-softmax update of
+// (m, l, o) and the P.V product.
+template <typename T, int HD>
+__device__ __forceinline__ void attn_block(const KVBlock<T, HD>& blk, int base, int limit, const u4* qf,
+                                           const u4* ql, float scale, float& mrun, float& lrun, f4* o) {
+  using B = KVBlock<T, HD>;
+  constexpr int KB = B::KB, ND = B::ND, TT = B::TT;
+  const int lane = threadIdx.x & 63, g = lane >> 4;
   float sc[KB / 4];
 #pragma unroll
   for (int t = 0; t < TT; ++t) {
-    const int slot = base + (r16 >> 2) * (KB / 4) + 4 * t + (r16 & 3);
-    const T* kp = Kb + (size_t)slot * HD + g * EPL;
     f4 s = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int f = 0; f < NF; ++f) mma_act_b<T>(s, ld16_stream(kp + f * KB), qf[f], ql[f]);
+    for (int f = 0; f < B::NF; ++f) mma_act_b<T>(s, blk.k[t][f], qf[f], ql[f]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int sl = base + g * (KB / 4) + 4 * t + i;
@@ -96,20 +122,43 @@ __device__ __forceinline__ void attn_block(const T* Kb, const T* Vb, int S, int 
   }
   u4 phi, plo;
   PFrag<T>::make(p, phi, plo);
-  const T* vp = Vb + (size_t)r16 * S + base + g * (KB / 4);
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) {
-    const u4 vf = ld16_stream(vp + (size_t)dt * 16 * S);
-    Frag<T>::mma(o[dt], phi, vf);
-    if constexpr (PFrag<T>::TWO) Frag<T>::mma(o[dt], plo, vf);
+    Frag<T>::mma(o[dt], phi, blk.v[dt]);
+    if constexpr (PFrag<T>::TWO) Frag<T>::mma(o[dt], plo, blk.v[dt]);
   }
 }
 
+// blocks [b0, b1) of KB slots from s0, limit `limit`; block i+1 loads while i computes
 template <typename T, int HD>
-__global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
+__device__ __forceinline__ void attn_range(const T* Kb, const T* Vb, int S, int s0, int b0, int b1, int limit,
+                                           const u4* qf, const u4* ql, float scale, float& mrun, float& lrun,
+                                           f4* o) {
+  constexpr int KB = Frag<T>::KB;
+  if (b0 >= b1) return;
+  KVBlock<T, HD> cur, nxt;
+  kv_load<T, HD>(cur, Kb, Vb, S, s0 + b0 * KB);
+  for (int bk = b0; bk < b1; ++bk) {
+    const bool more = bk + 1 < b1;
+    if (more) kv_load<T, HD>(nxt, Kb, Vb, S, s0 + (bk + 1) * KB);
+    attn_block<T, HD>(cur, s0 + bk * KB, limit, qf, ql, scale, mrun, lrun, o);
+    if (more) cur = nxt;
+  }
+}
+
+// One workgroup per (query row, kv head, slot split); its NW waves take
+// consecutive key blocks of the split's slot range and merge their (max, sum,
+// output) through LDS in wave order.  With one split the workgroup writes the
+// final output; otherwise it writes the split's partial for k_attn_combine.
+constexpr int ATTN_NW = 8;
+
+template <typename T, int HD>
+__global__ __launch_bounds__(64 * ATTN_NW) void k_attn_decode(AttnArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16;
-  const int lane = threadIdx.x, r16 = lane & 15, g = lane >> 4;
+  __shared__ float sO[ATTN_NW][4][HD];   // per wave: output rows of up to 4 q-heads (grp <= 4 here)
+  __shared__ float sM[ATTN_NW][16], sL[ATTN_NW][16];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
   const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
   const int grp = a.H / a.Hkv;
   const RowInfo ri = row_info(a.rm, r);
@@ -118,6 +167,9 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
   chunk = (chunk + KB - 1) / KB * KB;
   const int s0 = split * chunk;
   const int s1 = min(nval, s0 + chunk);
+  // this wave's key blocks: a contiguous share of the split's blocks
+  const int nblk = s1 > s0 ? (s1 - s0 + KB - 1) / KB : 0;
+  const int b0 = w * nblk / ATTN_NW, b1 = (w + 1) * nblk / ATTN_NW;
   const T* Kb = (const T*)a.K + ri.b * a.sb + kvh * a.sh;
   const T* Vb = (const T*)a.VT + ri.b * a.sb + kvh * a.sh;
   u4 qf[NF], ql[NF];
@@ -133,39 +185,49 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnArgs a) {
   for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
-  for (int base = s0; base < s1; base += KB)
-    attn_block<T, HD>(Kb, Vb, a.S, base, s1, qf, ql, scale, mrun, lrun, o);
+  attn_range<T, HD>(Kb, Vb, a.S, s0, b0, b1, s1, qf, ql, scale, mrun, lrun, o);
 
-  if (a.nsplit == 1) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = 4 * g + i;
-      const float lj = __shfl(lrun, j & 15, WAVE);
-      if (j < grp) {
-        const int c0 = (kvh * grp + j) * HD + r16;
-        const float inv = lj > 0.f ? 1.0f / lj : 0.f;
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, r, a.ldo, c0 + dt * 16, o[dt][i] * inv);
-      }
-    }
-    return;
+  // publish this wave's state; rows 4g+i of the output live in lane group g
+  if (g == 0) {
+    sM[w][r16] = mrun;
+    sL[w][r16] = lrun;
   }
-  // publish (m, l, O) of this split: part[r][kvh][split][j][HD + 2]
-  const size_t rec = HD + 2;
-  float* pb = a.part + (((size_t)r * a.Hkv + kvh) * a.nsplit) * grp * rec;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * g + i;
     if (j < grp) {
-      float* pj = pb + ((size_t)split * grp + j) * rec;
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) pj[dt * 16 + r16] = o[dt][i];
+      for (int dt = 0; dt < ND; ++dt) sO[w][j][dt * 16 + r16] = o[dt][i];
     }
   }
-  if (r16 < grp && g == 0) {
-    float* pj = pb + ((size_t)split * grp + r16) * rec;
-    pj[HD] = mrun;
-    pj[HD + 1] = lrun;
+  __syncthreads();
+  // merge the waves in order: each thread owns (head j, column d) pairs
+  const size_t rec = HD + 2;
+  float* pb = a.part + (((size_t)r * a.Hkv + kvh) * a.nsplit) * grp * rec;
+  for (int t = threadIdx.x; t < grp * HD; t += 64 * ATTN_NW) {
+    const int j = t / HD, d = t % HD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < ATTN_NW; ++q) M = fmaxf(M, sM[q][j]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < ATTN_NW; ++q) {
+        const float wgt = sM[q][j] == -INFINITY ? 0.f : __expf(sM[q][j] - M);
+        L += wgt * sL[q][j];
+        O += wgt * sO[q][j][d];
+      }
+    }
+    if (a.nsplit == 1) {
+      Act<T>::put(a.o, r, a.ldo, (kvh * grp + j) * HD + d, L > 0.f ? O / L : 0.f);
+    } else {
+      float* pj = pb + ((size_t)split * grp + j) * rec;
+      pj[d] = O;
+      if (d == 0) {
+        pj[HD] = M;
+        pj[HD + 1] = L;
+      }
+    }
   }
 }
 
@@ -223,10 +285,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
   for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
-  for (int base = 0; base < wave_end; base += KB) {
-    // per-lane limit: the score mask uses this lane's query row (r16)
-    attn_block<T, HD>(Kb, Vb, a.S, base, limit, qf, ql, scale, mrun, lrun, o);
-  }
+  // per-lane limit: the score mask uses this lane's query row (r16)
+  attn_range<T, HD>(Kb, Vb, a.S, 0, 0, (wave_end + KB - 1) / KB, limit, qf, ql, scale, mrun, lrun, o);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * g + i;  // query row within the wave
@@ -242,8 +302,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
 template <typename T>
 static int decode_t(const AttnArgs& a, Stream s) {
   dim3 grid(a.nsplit, a.Hkv, a.R);
-  if (a.hd == 64) hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64), 0, s, a);
-  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64), 0, s, a);
+  if (a.hd == 64) hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else return -1;
   if (a.nsplit > 1) hipLaunchKernelGGL((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, a);
   return 0;
@@ -258,7 +318,7 @@ static int prefill_t(const AttnArgs& a, Stream s) {
 }
 
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s) {
-  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 16 || a.S % 64 != 0) return -1;
+  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 4 || a.S % 64 != 0) return -1;
   return dtype == 1 ? decode_t<bf16>(a, s) : decode_t<float>(a, s);
 }
 int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s) {

@@ -14,39 +14,77 @@ namespace ham {
 // ---------------------------------------------------------------- RMSNorm
 // out[r] = g * x / sqrt(mean(x^2) + eps), rounded to the storage type (the GEMM operand)
 // A pending split-K result of the previous GEMM (partials) is first added to the
-// residual row in split order, and the updated row optionally copied out.
+// residual row in split order, and the updated row optionally copied out.  One
+// 1024-thread block per row: every thread owns d/1024 columns and issues all of
+// its partial loads before summing them.
+constexpr int NORM_THREADS = 1024;
+constexpr int NORM_MAXV = 8;  // d <= 8192
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a) {
+__global__ __launch_bounds__(NORM_THREADS) void k_rmsnorm(NormArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
-  __shared__ float sh[4];
+  __shared__ float sh[NORM_THREADS / 64];
   const int r = blockIdx.x;
   const int xr = r * a.row_stride + a.row_off;
   float* x = a.x + (size_t)xr * a.ldx;
+  float v[NORM_MAXV];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < a.d; i += 256) {
-    float v = x[i];
-    if (a.part) {
-      float p = 0.f;
-      for (int s = 0; s < a.nsplit; ++s) p += a.part[((size_t)s * a.pM + xr) * a.ldx + i];
-      v += p;
-      x[i] = v;
-    }
-    if (a.ctx) a.ctx[(size_t)r * a.ldctx + i] = v;
-    ss += v * v;
+#pragma unroll
+  for (int e = 0; e < NORM_MAXV; ++e) {
+    const int i = threadIdx.x + e * NORM_THREADS;
+    v[e] = 0.f;
+    if (i < a.d) v[e] = x[i];
   }
-  ss = block_sum256(ss, sh);
-  const float inv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
-  for (int i = threadIdx.x; i < a.d; i += 256) {
-    const float v = x[i] * inv * a.g[i];
-    Act<T>::put(a.out, r, a.ldo, i, v);
-    if (a.hid) a.hid[(size_t)r * a.ldh + i] = v;
+  if (a.part) {
+    const size_t sstride = (size_t)a.pM * a.ldx;
+    const float* pp = a.part + (size_t)xr * a.ldx;
+#pragma unroll
+    for (int e = 0; e < NORM_MAXV; ++e) {
+      const int i = threadIdx.x + e * NORM_THREADS;
+      if (i < a.d) {
+        float p[4] = {0.f, 0.f, 0.f, 0.f};
+        int s = 0;
+        for (; s + 4 <= a.nsplit; s += 4) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) p[q] += pp[(size_t)(s + q) * sstride + i];
+        }
+        for (; s < a.nsplit; ++s) p[0] += pp[(size_t)s * sstride + i];
+        v[e] += ((p[0] + p[1]) + (p[2] + p[3]));
+        x[i] = v[e];
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < NORM_MAXV; ++e) {
+    const int i = threadIdx.x + e * NORM_THREADS;
+    if (i < a.d) {
+      if (a.ctx) a.ctx[(size_t)r * a.ldctx + i] = v[e];
+      ss += v[e] * v[e];
+    }
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int q = 0; q < NORM_THREADS / 64; ++q) tot += sh[q];
+  const float inv = 1.0f / sqrtf(tot / (float)a.d + a.eps);
+#pragma unroll
+  for (int e = 0; e < NORM_MAXV; ++e) {
+    const int i = threadIdx.x + e * NORM_THREADS;
+    if (i < a.d) {
+      const float o = v[e] * inv * a.g[i];
+      Act<T>::put(a.out, r, a.ldo, i, o);
+      if (a.hid) a.hid[(size_t)r * a.ldh + i] = o;
+    }
   }
 }
 
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
   if (a.R <= 0) return 0;
-  if (dtype == 1) hipLaunchKernelGGL((k_rmsnorm<bf16>), dim3(a.R), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((k_rmsnorm<float>), dim3(a.R), dim3(256), 0, s, a);
+  if (a.d > NORM_THREADS * NORM_MAXV) return -1;
+  if (dtype == 1) hipLaunchKernelGGL((k_rmsnorm<bf16>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
+  else hipLaunchKernelGGL((k_rmsnorm<float>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
   return 0;
 }
 

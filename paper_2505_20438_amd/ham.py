@@ -21,7 +21,8 @@ HAM_PROF_KINDS = 9
 
 EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
             "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
-            "ham_tensor_info", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy")
+            "ham_tensor_info", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
+            "ham_op_attention_workspace_bytes", "ham_op_decode_attention")
 
 
 class HamConfig(ctypes.Structure):
@@ -80,6 +81,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(I32)]
     lib.ham_profile.argtypes = [P, I32]
     lib.ham_profile_read.argtypes = [P, ctypes.POINTER(HamProfT), I32]
+    lib.ham_op_attention_workspace_bytes.argtypes = [I32, I32, I32, I32]
+    lib.ham_op_attention_workspace_bytes.restype = SZ
+    lib.ham_op_decode_attention.argtypes = [I32, I32, I32, I32, I32, I32, P, P, P, P, P, I32, P, P, SZ, P]
+    lib.ham_op_decode_attention.restype = I32
     lib.ham_last_error.restype = ctypes.c_char_p
     lib.ham_destroy.argtypes = [P]
     lib.ham_destroy.restype = None
@@ -159,6 +164,20 @@ def ham_kv_stats(model: int, batch: int) -> List[dict]:
 
 def ham_set_debug(model: int, buf) -> None:
     _check(load_library().ham_set_debug(model, _ptr(buf), 0 if buf is None else buf.numel() * buf.element_size()))
+
+
+def ham_op_decode_attention(dtype: int, q, k, vt, kv_len, enable, kv_max: int, out, workspace, stream: int,
+                            n_heads: int, n_kv_heads: int, head_dim: int, slots_cap: int) -> None:
+    """Decode attention of one act row per sequence (include/ham_ops.h)."""
+    rows = kv_len.numel()
+    check(load_library().ham_op_decode_attention(
+        dtype, rows, n_heads, n_kv_heads, head_dim, slots_cap, q.data_ptr(), k.data_ptr(), vt.data_ptr(),
+        kv_len.data_ptr(), enable.data_ptr(), kv_max, out.data_ptr(), workspace.data_ptr(),
+        workspace.numel() * workspace.element_size(), stream))
+
+
+def ham_op_attention_workspace_bytes(rows: int, n_heads: int, n_kv_heads: int, head_dim: int) -> int:
+    return load_library().ham_op_attention_workspace_bytes(rows, n_heads, n_kv_heads, head_dim)
 
 
 def ham_steps_done(model: int) -> int:

@@ -1,0 +1,123 @@
+"""The C ABI on the CPU: the library loads, exports what include/*.h declares,
+and rejects bad configurations and calls before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2505_20438_amd import ham
+from synth.configs import SHAPE_1B, SHAPE_8B, TINY, WORKLOADS
+from tests.gpu_util import config_for
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ham.LIB_PATH):
+        pytest.skip("libham.so not built")
+    return ham.load_library()
+
+
+def _declared():
+    names = set()
+    for h in ("ham.h", "ham_ops.h"):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(ham_[a-z_0-9]+)\s*\(", text))
+    return names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    declared = _declared()
+    assert {"ham_init_weights", "ham_prefill", "ham_macro_step", "ham_kv_stats"} <= declared
+    for n in declared:
+        assert hasattr(lib, n), n
+    assert declared == set(ham.EXPORTED)
+
+
+def test_size_queries(lib):
+    for w in WORKLOADS.values():
+        cfg = config_for(w.shape, w.batch, w.prompt_len, max(w.max_new, w.macro_steps))
+        assert ham.ham_weights_bytes(cfg) > 0 and ham.ham_state_bytes(cfg) > 0
+        assert ham.ham_workspace_bytes(cfg) > 0
+    # the weights buffer holds at least every parameter once
+    cfg = config_for(SHAPE_8B, 1, 16, 16)
+    s = SHAPE_8B
+    layer = (2 * s.d_model * s.n_heads * s.head_dim + 2 * s.d_model * s.n_kv_heads * s.head_dim
+             + 3 * s.d_model * s.ffn_dim)
+    params = (s.n_layers + s.micro_layers) * layer + 2 * s.vocab * s.d_model + 5 * s.d_model ** 2
+    assert ham.ham_weights_bytes(cfg) >= 2 * params
+    # the smashed KV cache holds max_prompt + max_steps slots per sequence and layer
+    cfg = config_for(SHAPE_1B, 2, 100, 28)
+    kv = 2 * SHAPE_1B.n_layers * 2 * SHAPE_1B.n_kv_heads * 128 * SHAPE_1B.head_dim * 2
+    assert ham.ham_state_bytes(cfg) >= kv
+
+
+@pytest.mark.parametrize("field,value", [
+    ("head_dim", 96), ("n_kv_heads", 3), ("n_heads", 32), ("max_group", 5), ("max_group", 0), ("stop_mode", 7),
+    ("dtype", 3), ("max_batch", 0), ("max_batch", 65), ("ffn_dim", 700), ("d_model", 100), ("vocab", 1),
+    ("stop_conf", 1.5), ("micro_layers", 0), ("max_prompt", 0), ("norm_eps", 0.0)])
+def test_invalid_configs_are_rejected(lib, field, value):
+    cfg = config_for(TINY, 1, 8, 4)
+    setattr(cfg, field, value)
+    assert ham.ham_weights_bytes(cfg) == 0
+    h = ctypes.c_void_p()
+    rc = lib.ham_init_weights(ctypes.byref(cfg), 1, 256, 1 << 30, 256, 1 << 30, 256, 1 << 30, None, ctypes.byref(h))
+    assert rc == ham.HAM_EINVAL and h.value is None
+    assert len(lib.ham_last_error()) > 0
+
+
+def test_token_mode_stop_id_must_be_in_vocab(lib):
+    cfg = config_for(TINY, 1, 8, 4)
+    cfg.stop_id = TINY.vocab
+    assert ham.ham_weights_bytes(cfg) == 0
+
+
+def test_null_and_small_buffers(lib):
+    cfg = config_for(TINY, 1, 8, 4)
+    h = ctypes.c_void_p()
+    assert lib.ham_init_weights(ctypes.byref(cfg), 1, None, 0, None, 0, None, 0, None, ctypes.byref(h)) == ham.HAM_EINVAL
+    rc = lib.ham_init_weights(ctypes.byref(cfg), 1, 256, 16, 256, 16, 256, 16, None, ctypes.byref(h))
+    assert rc == ham.HAM_ENOMEM
+    assert b"too small" in lib.ham_last_error()
+    rc = lib.ham_init_weights(ctypes.byref(cfg), 1, 257, 1 << 40, 256, 1 << 40, 256, 1 << 40, None, ctypes.byref(h))
+    assert rc == ham.HAM_EINVAL  # misaligned
+
+
+def test_calls_on_null_handle(lib):
+    assert lib.ham_macro_step(None, None, None, None, None) == ham.HAM_EINVAL
+    assert lib.ham_prefill(None, 1, None, 1, None, None, None, None, None) == ham.HAM_EINVAL
+    assert lib.ham_kv_stats(None, None) == ham.HAM_EINVAL
+    assert lib.ham_steps_done(None) == -1
+    lib.ham_destroy(None)
+
+
+def test_tensor_info_layout(lib):
+    cfg = config_for(TINY, 1, 8, 4)
+    seen = []
+    ids = list(range(9)) + [16 + 8 * j + t for j in range(TINY.n_layers + TINY.micro_layers) for t in range(7)]
+    for tid in ids:
+        off, rows, cols, inter = ham.ham_tensor_info(cfg, tid)
+        assert off % 256 == 0 or tid in (3, 4, 8) or (tid >= 16 and (tid - 16) % 8 in (1, 2, 5))
+        assert off + rows * cols * 4 <= ham.ham_weights_bytes(cfg)
+        seen.append((off, rows, cols, inter))
+    assert seen[0][1:3] == (TINY.vocab, TINY.d_model)
+    wg, wu = seen[9 + 4], seen[9 + 5]
+    assert wg[0] == wu[0] and (wg[3], wu[3]) == (1, 2) and wg[1] == TINY.ffn_dim
+    with pytest.raises(ham.HamError):
+        ham.ham_tensor_info(cfg, 12)
+    with pytest.raises(ham.HamError):
+        ham.ham_tensor_info(cfg, 16 + 8 * 3)
+
+
+def test_op_attention_rejects_bad_shapes(lib):
+    assert ham.ham_op_attention_workspace_bytes(1, 32, 8, 128) > 0
+    ws = 1 << 20
+    rc = lib.ham_op_decode_attention(1, 1, 32, 8, 96, 64, 256, 256, 256, 256, 256, 8, 256, 256, ws, None)
+    assert rc == ham.HAM_EINVAL
+    rc = lib.ham_op_decode_attention(1, 1, 32, 8, 128, 100, 256, 256, 256, 256, 256, 8, 256, 256, ws, None)
+    assert rc == ham.HAM_EINVAL
+    rc = lib.ham_op_decode_attention(1, 4, 32, 8, 128, 4096, 256, 256, 256, 256, 256, 8, 256, 256, 16, None)
+    assert rc == ham.HAM_ENOMEM

@@ -147,15 +147,19 @@ int ham_set_debug(ham_model* m, void* d_buf, size_t bytes);
 /* Number of macro-steps run since the last prefill, or -1. */
 int ham_steps_done(const ham_model* m);
 
-/* Offset (bytes) and shape of one generated tensor inside the weights buffer,
- * by the tensor id used by the initialiser (see DESIGN notes of the generator:
- * 0 E, 1 P, 2..6 A_q A_k A_v A_o A_lin, 7 LM head, 8 stop head, 16 + 8j + t for
- * layer j, t = 0..6 Wq Wk Wv Wo Wgate Wup Wdown).  Row r of the tensor is stored
- * at offset + row_pos(r) * cols * elem_size, where row_pos is the identity
- * except for Wgate/Wup, which are interleaved in blocks of 16 rows
- * (*interleave = 1: gate rows at 32*(r/16) + r%16, up rows 16 later). */
-int ham_tensor_info(const ham_config* cfg, int32_t tensor_id, size_t* offset, int32_t* rows,
-                    int32_t* cols, int32_t* interleave);
+/* Where one generated tensor lives in the weights buffer, by the tensor id of
+ * the initialiser (0 E, 1 P, 2..6 A_q A_k A_v A_o A_lin, 7 LM head, 8 stop
+ * head, 16 + 8j + t for layer j (base layers first, then micro layers),
+ * t = 0..6 Wq Wk Wv Wo Wgate Wup Wdown).  The tensor [rows][cols] is part of a
+ * stored matrix of mat_rows rows starting at `offset`: its row r is matrix row
+ * row_off + r, except for Wgate/Wup (*interleave 1/2), whose rows are
+ * interleaved in blocks of 8 (gate row r at 16*(r/8) + r%8, up row 8 later).
+ * Matrices with *tiled = 1 are stored fragment-tiled: element (n, k) of a
+ * bf16 matrix with K columns is at
+ *   ((n/16 * K/32 + k/32) * 64 + ((k%32)/8) * 16 + n%16) * 8 + k%8
+ * (fp32: 16-column fragments of 4 elements per lane); E and P are row-major. */
+int ham_tensor_info(const ham_config* cfg, int32_t tensor_id, size_t* offset, int32_t* rows, int32_t* cols,
+                    int32_t* row_off, int32_t* mat_rows, int32_t* interleave, int32_t* tiled);
 
 /* Per-kernel-class timing of later calls (diagnostics for the benchmark).
  * While enabled, every launch of the classes below is bracketed by a pair of

@@ -82,6 +82,18 @@ template <> struct Act<bf16> {
   }
 };
 
+// Fragment-tiled weight layout.  A weight matrix W [N][K] (N a multiple of 16,
+// K of the fragment width KB) is stored as 1 KB blocks, one per (16-row tile,
+// KB-column fragment), in the order the lanes of a wave read them: lane
+// l = 16*g + r holds row r of the tile and elements [g*EPL, g*EPL + EPL) of the
+// fragment.  A wave then streams each block with one fully contiguous 1 KB load.
+template <typename T>
+__host__ __device__ __forceinline__ size_t tiled_index(size_t n, size_t k, size_t K) {
+  constexpr int EPL = 16 / sizeof(T), KB = 4 * EPL;
+  const size_t nt = n / 16, r = n % 16, f = k / KB, kk = k % KB, g = kk / EPL, e = kk % EPL;
+  return ((nt * (K / KB) + f) * 64 + g * 16 + r) * EPL + e;
+}
+
 __device__ __forceinline__ u4 ld16(const void* p) { return *reinterpret_cast<const u4*>(p); }
 // streamed once per step (weights, KV): non-temporal hint so they do not displace reused lines
 __device__ __forceinline__ u4 ld16_stream(const void* p) {

@@ -153,8 +153,8 @@ Layout make_layout(const ham_config* c) {
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);
   y.apart = take(attn_part_bytes(y.rows_dec, y.H, y.Hk, y.hd));
-  y.bval = take((size_t)(y.Vpad / 32) * 64 * 4);
-  y.bidx = take((size_t)(y.Vpad / 32) * 64 * 4);
+  y.bval = take((size_t)(y.Vpad / 16) * 64 * 4);
+  y.bidx = take((size_t)(y.Vpad / 16) * 64 * 4);
   y.stopb = take(64 * 4);
   y.ctx = take((size_t)y.B * y.C * y.d * 4);
   y.emb_in = take((size_t)5 * y.B * y.d * 4);
@@ -351,7 +351,7 @@ int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, con
   int ns = 1;
   if (gemm_p(m, EPI_ARGMAX, ga, 1, k == 0 ? HAM_PROF_HEAD0 : HAM_PROF_HEADK, &ns))
     return fail(HAM_EINVAL, "lm head shape");
-  launch_decide(d, y.Vpad / 32, B, m->s);
+  launch_decide(d, skinny_tiles(y.Vpad), B, m->s);
   return HAM_OK;
 }
 
@@ -415,34 +415,39 @@ size_t ham_state_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_lay
 size_t ham_workspace_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_layout(c).ws_bytes; }
 
 int ham_tensor_info(const ham_config* c, int32_t id, size_t* offset, int32_t* rows, int32_t* cols,
-                    int32_t* interleave) {
+                    int32_t* row_off, int32_t* mat_rows, int32_t* interleave, int32_t* tiled) {
   if (const char* e = check_cfg(c)) return fail(HAM_EINVAL, "%s", e);
-  if (!offset || !rows || !cols || !interleave) return fail(HAM_EINVAL, "null output pointer");
+  if (!offset || !rows || !cols || !row_off || !mat_rows || !interleave || !tiled)
+    return fail(HAM_EINVAL, "null output pointer");
   const Layout y = make_layout(c);
   *interleave = 0;
-  const size_t es = y.es;
+  *row_off = 0;
+  *tiled = 1;
+  auto set = [&](size_t off, int r, int cl, int roff, int mrows) {
+    *offset = off; *rows = r; *cols = cl; *row_off = roff; *mat_rows = mrows;
+  };
   switch (id) {
-    case 0: *offset = y.E; *rows = y.V; *cols = y.d; return HAM_OK;
-    case 1: *offset = y.Pe; *rows = 4; *cols = y.d; return HAM_OK;
-    case 2: case 3: case 4:
-      *offset = y.Aqkv + (size_t)(id - 2) * y.HD * y.d * es; *rows = y.HD; *cols = y.d; return HAM_OK;
-    case 5: *offset = y.Ao; *rows = y.d; *cols = y.HD; return HAM_OK;
-    case 6: *offset = y.Alin; *rows = y.d; *cols = y.d; return HAM_OK;
-    case 7: *offset = y.Wlm; *rows = y.V; *cols = y.d; return HAM_OK;
-    case 8: *offset = y.Wlm + (size_t)y.V * y.d * es; *rows = 1; *cols = y.d; return HAM_OK;
+    case 0: set(y.E, y.V, y.d, 0, y.V); *tiled = 0; return HAM_OK;
+    case 1: set(y.Pe, 4, y.d, 0, 4); *tiled = 0; return HAM_OK;
+    case 2: case 3: case 4: set(y.Aqkv, y.HD, y.d, (id - 2) * y.HD, 3 * y.HD); return HAM_OK;
+    case 5: set(y.Ao, y.d, y.HD, 0, y.d); return HAM_OK;
+    case 6: set(y.Alin, y.d, y.d, 0, y.d); return HAM_OK;
+    case 7: set(y.Wlm, y.V, y.d, 0, y.Vpad); return HAM_OK;
+    case 8: set(y.Wlm, 1, y.d, y.V, y.Vpad); return HAM_OK;
     default: break;
   }
   if (id < 16) return fail(HAM_EINVAL, "unknown tensor id %d", id);
   const int j = (id - 16) / 8, t = (id - 16) % 8;
   if (j >= y.L + y.M || t > 6) return fail(HAM_EINVAL, "unknown tensor id %d", id);
+  const int kvd = y.Hk * y.hd;
   switch (t) {
-    case 0: *offset = y.Wqkv[j]; *rows = y.HD; *cols = y.d; break;
-    case 1: *offset = y.Wqkv[j] + (size_t)y.HD * y.d * es; *rows = y.Hk * y.hd; *cols = y.d; break;
-    case 2: *offset = y.Wqkv[j] + (size_t)(y.HD + y.Hk * y.hd) * y.d * es; *rows = y.Hk * y.hd; *cols = y.d; break;
-    case 3: *offset = y.Wo[j]; *rows = y.d; *cols = y.HD; break;
-    case 4: *offset = y.Wgu[j]; *rows = y.F; *cols = y.d; *interleave = 1; break;
-    case 5: *offset = y.Wgu[j]; *rows = y.F; *cols = y.d; *interleave = 2; break;
-    case 6: *offset = y.Wd[j]; *rows = y.d; *cols = y.F; break;
+    case 0: set(y.Wqkv[j], y.HD, y.d, 0, y.QKV); break;
+    case 1: set(y.Wqkv[j], kvd, y.d, y.HD, y.QKV); break;
+    case 2: set(y.Wqkv[j], kvd, y.d, y.HD + kvd, y.QKV); break;
+    case 3: set(y.Wo[j], y.d, y.HD, 0, y.d); break;
+    case 4: set(y.Wgu[j], y.F, y.d, 0, 2 * y.F); *interleave = 1; break;
+    case 5: set(y.Wgu[j], y.F, y.d, 0, 2 * y.F); *interleave = 2; break;
+    case 6: set(y.Wd[j], y.d, y.F, 0, y.d); break;
   }
   return HAM_OK;
 }
@@ -480,14 +485,15 @@ int ham_init_weights(const ham_config* c, uint64_t seed, void* d_weights, size_t
   INIT_TRY(hipMemsetAsync(d_weights, 0, y.w_bytes, s));
   INIT_TRY(hipMemsetAsync(d_state, 0, y.st_bytes, s));
   INIT_TRY(hipMemsetAsync(d_workspace, 0, y.ws_bytes, s));
-  auto gen = [&](size_t off, int rows, int cols, long long row_off, int inter, int tid) {
+  // every GEMM weight matrix is stored fragment-tiled; E and P (row gathers) row-major
+  auto gen = [&](size_t off, int rows, int cols, long long row_off, int inter, int tid, int tiled = 1) {
     GenArgs g{};
     g.dst = m->w + off; g.rows = rows; g.cols = cols; g.row_off = row_off; g.interleave = inter;
-    g.key = sm64(seed, (uint64_t)tid);
+    g.tiled = tiled; g.key = sm64(seed, (uint64_t)tid);
     launch_gen_normal(dt, g, s);
   };
-  gen(y.E, y.V, y.d, 0, 0, 0);
-  gen(y.Pe, 4, y.d, 0, 0, 1);
+  gen(y.E, y.V, y.d, 0, 0, 0, 0);
+  gen(y.Pe, 4, y.d, 0, 0, 1, 0);
   for (int i = 0; i < 3; ++i) gen(y.Aqkv, y.HD, y.d, (long long)i * y.HD, 0, 2 + i);
   gen(y.Ao, y.d, y.HD, 0, 0, 5);
   gen(y.Alin, y.d, y.d, 0, 0, 6);

@@ -86,6 +86,7 @@ typedef hipStream_t Stream;
 // *nsplit receives the k-split used; above 1 the result is fp32 partials in a.part.
 int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, int tag, int* nsplit);
 int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s);
+int skinny_tiles(int N);  // column tiles (argmax partials per row) of a skinny launch over N columns
 int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s);
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s);
 int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s);

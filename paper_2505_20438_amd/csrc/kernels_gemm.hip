@@ -1,12 +1,13 @@
 // Weight GEMMs of the decode loop: C[m][n] = sum_k X[m][k] * W[n][k].
 //
-// Two matrix-core kernels share one set of fused epilogues:
+// Weights are stored fragment-tiled (device_common.h): every wave load of a
+// weight fragment is one contiguous 1 KB block.  Two matrix-core kernels share
+// one set of fused epilogues:
 //  * k_gemm_skinny (M <= 64 rows: decode, micro steps, LM head).  HBM-bound
-//    weight streaming: each lane loads 16 contiguous bytes of a weight row per
-//    fragment with a non-temporal hint, four waves split the k-range of a
-//    32-column tile, and loads of the next batch of fragments are issued before
-//    the matrix instructions of the current one.  The k dimension may also be
-//    split across workgroups: each split then writes fp32 partials
+//    weight streaming with non-temporal loads; four waves split the k-range of
+//    a 16*TN-column tile, and loads of the next batch of fragments are issued
+//    before the matrix instructions of the current one.  The k dimension may
+//    also be split across workgroups: each split then writes fp32 partials
 //    [split][M][N] and the consuming kernel sums them in split order (no
 //    cross-workgroup synchronisation inside a kernel: on this GPU the L2 of one
 //    XCD is not coherent with the others, and the write-back fences that a
@@ -14,7 +15,8 @@
 //  * k_gemm_big (M > 64: prefill chunks, batched micro context rows): 128x128
 //    LDS-staged tiles, double buffered, 2x2 waves of 64x64.
 // X rows are the A operand (padded to 16), weight rows the B operand, so the
-// accumulator's columns are output features.
+// accumulator's columns are output features: lane l holds column l & 15 of a
+// 16-column tile for rows 4*(l >> 4) + i.
 #include <algorithm>
 
 #include "decide.h"
@@ -23,31 +25,30 @@
 
 namespace ham {
 
+// Epilogue of one accumulator element: row m, column nb + r16 of the tile at nb.
+// Every lane must call it (the SwiGLU pairing exchanges values between lanes).
 template <typename T, int EPI>
-__device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int nb, int r16, float ve, float vo) {
-  const int ne = nb + r16, no = nb + 16 + r16;
-  if constexpr (EPI == EPI_F32) {
-    float* o = (float*)a.out + (size_t)m * a.ldo;
-    o[ne] = ve;
-    o[no] = vo;
-  } else if constexpr (EPI == EPI_OP) {
-    Act<T>::put(a.out, m, a.ldo, ne, ve);
-    Act<T>::put(a.out, m, a.ldo, no, vo);
-  } else if constexpr (EPI == EPI_RESID) {
-    float* o = (float*)a.out + (size_t)m * a.ldo;
-    const float xe = o[ne] + ve, xo = o[no] + vo;
-    o[ne] = xe;
-    o[no] = xo;
-  } else if constexpr (EPI == EPI_XMASK) {
-    if (a.rowmask[m]) {
-      float* o = (float*)a.out + (size_t)m * a.ldo;
-      o[ne] = ve;
-      o[no] = vo;
+__device__ __forceinline__ void epi_tile(const GemmArgs& a, int m, bool ok, int nb, int r16, float v) {
+  const int n = nb + r16;
+  if constexpr (EPI == EPI_SWIGLU) {
+    // a 16-row tile holds gate rows of 8 features then their up rows
+    const float u = __shfl_xor(v, 8, WAVE);
+    if (ok && r16 < 8) {
+      const float sg = v / (1.0f + expf(-v));
+      Act<T>::put(a.out, m, a.ldo, nb / 2 + r16, sg * u);
     }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    // gate rows and up rows are interleaved in blocks of 16: pair (gate, up) of feature f
-    const float sg = ve / (1.0f + expf(-ve));
-    Act<T>::put(a.out, m, a.ldo, nb / 2 + r16, sg * vo);
+  } else {
+    if (!ok) return;
+    if constexpr (EPI == EPI_F32) {
+      ((float*)a.out)[(size_t)m * a.ldo + n] = v;
+    } else if constexpr (EPI == EPI_OP) {
+      Act<T>::put(a.out, m, a.ldo, n, v);
+    } else if constexpr (EPI == EPI_RESID) {
+      float* o = (float*)a.out + (size_t)m * a.ldo;
+      o[n] += v;
+    } else if constexpr (EPI == EPI_XMASK) {
+      if (a.rowmask[m]) ((float*)a.out)[(size_t)m * a.ldo + n] = v;
+    }
   }
 }
 
@@ -56,21 +57,22 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
 }
 
 // ------------------------------------------------------------------------ skinny
-template <typename T, int MT>
+template <typename T, int MT, int TN>
 struct SkinnyBatch {
   static constexpr int U = 4;
-  u4 w[U][2];
+  u4 w[U][TN];
   u4 xh[U][MT], xl[U][MT];
 };
 
-template <typename T, int MT>
-__device__ __forceinline__ void skinny_load(SkinnyBatch<T, MT>& b, const T* const* wrow, const T* const* xrow,
+// fragment f of every operand: weight block (tile j, f) at wrow[j] + f*512 elements-of-16B
+template <typename T, int MT, int TN>
+__device__ __forceinline__ void skinny_load(SkinnyBatch<T, MT, TN>& b, const T* const* wrow, const T* const* xrow,
                                             const bool* xok, int lo_off, int f) {
-  constexpr int KB = Frag<T>::KB, U = SkinnyBatch<T, MT>::U;
+  constexpr int KB = Frag<T>::KB, EPL = Frag<T>::EPL, U = SkinnyBatch<T, MT, TN>::U;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) b.w[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * KB);
+    for (int j = 0; j < TN; ++j) b.w[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * 64 * EPL);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       const u4 h = ld16(xrow[i] + (size_t)(f + u) * KB);
@@ -83,25 +85,24 @@ __device__ __forceinline__ void skinny_load(SkinnyBatch<T, MT>& b, const T* cons
   }
 }
 
-template <typename T, int MT>
-__device__ __forceinline__ void skinny_mma(f4 (*acc)[2], const SkinnyBatch<T, MT>& b) {
+template <typename T, int MT, int TN>
+__device__ __forceinline__ void skinny_mma(f4 (*acc)[TN], const SkinnyBatch<T, MT, TN>& b) {
 #pragma unroll
-  for (int u = 0; u < SkinnyBatch<T, MT>::U; ++u)
+  for (int u = 0; u < SkinnyBatch<T, MT, TN>::U; ++u)
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) mma_act<T>(acc[i][j], b.xh[u][i], b.xl[u][i], b.w[u][j]);
+      for (int j = 0; j < TN; ++j) mma_act<T>(acc[i][j], b.xh[u][i], b.xl[u][i], b.w[u][j]);
 }
 
 // TAG only separates the names of base-layer launches (always active) from the
 // others in profiler output; the code is the same.
-template <typename T, int MT, int EPI, int TAG>
+template <typename T, int MT, int TN, int EPI, int TAG>
 __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
-  constexpr int TN = 2;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB;
   constexpr int NACC = MT * TN * 4;
-  constexpr int U = SkinnyBatch<T, MT>::U;
+  constexpr int U = SkinnyBatch<T, MT, TN>::U;
   __shared__ float red[3][NACC][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
 
   const T* wrow[TN];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) wrow[j] = W + (size_t)(n0 + 16 * j + r16) * a.K + g * EPL;
+  for (int j = 0; j < TN; ++j) wrow[j] = W + (size_t)(n0 / 16 + j) * nfr * 64 * EPL + (size_t)lane * EPL;
   constexpr int PL = Act<T>::PL;
   const int lo_off = Act<T>::SPLIT ? a.ldx : 0;  // offset of the lo plane within a row
   const T* xrow[MT];
@@ -136,18 +137,18 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   // software pipeline over batches of U fragments: the loads of batch i+1 are
   // in flight while batch i feeds the matrix cores
   const int nb = (f1 - f0) / U;
-  SkinnyBatch<T, MT> cur, nxt;
-  if (nb > 0) skinny_load<T, MT>(cur, wrow, xrow, xok, lo_off, f0);
+  SkinnyBatch<T, MT, TN> cur, nxt;
+  if (nb > 0) skinny_load<T, MT, TN>(cur, wrow, xrow, xok, lo_off, f0);
   for (int it = 0; it < nb; ++it) {
     const bool more = it + 1 < nb;
-    if (more) skinny_load<T, MT>(nxt, wrow, xrow, xok, lo_off, f0 + (it + 1) * U);
-    skinny_mma<T, MT>(acc, cur);
+    if (more) skinny_load<T, MT, TN>(nxt, wrow, xrow, xok, lo_off, f0 + (it + 1) * U);
+    skinny_mma<T, MT, TN>(acc, cur);
     if (more) cur = nxt;
   }
   for (int f = f0 + nb * U; f < f1; ++f) {
     u4 bw[TN];
 #pragma unroll
-    for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * KB);
+    for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * 64 * EPL);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       u4 h = ld16(xrow[i] + (size_t)f * KB), l = zero16();
@@ -232,10 +233,12 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = 16 * i + 4 * g + r;
-        if (m < a.M) epi_pair<T, EPI>(a, m, n0, r16, acc[i][0][r], acc[i][1][r]);
-      }
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 16 * i + 4 * g + r;
+          epi_tile<T, EPI>(a, m, m < a.M, n0 + 16 * j, r16, acc[i][j][r]);
+        }
   }
 }
 
@@ -306,11 +309,24 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
   const T* W = (const T*)a.W;
   const T* X = (const T*)a.X;
   const int lr = tid >> 1, lc = (tid & 1) * 2;
-  const bool aok = m0 + lr < a.M, bok = n0 + lr < a.N;
+  const bool aok = m0 + lr < a.M;
   const T* ap = X + (size_t)(aok ? m0 + lr : 0) * a.ldx * NA + lc * EPL;
-  const T* bp = W + (size_t)(bok ? n0 + lr : 0) * a.K + lc * EPL;
+  // B tile: 8 fragment blocks (16 rows x KB each, 64 u4 in lane order) per stage;
+  // thread t copies u4 number 2t and 2t+1 of the 512
+  const int nfr = a.K / KB;
+  int bidx[2], brow[2], bg[2];
+  bool bok[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int u = 2 * tid + q, blk = u >> 6, l = u & 63;
+    brow[q] = blk * 16 + (l & 15);
+    bg[q] = l >> 4;
+    bok[q] = n0 + blk * 16 < a.N;
+    bidx[q] = l;
+  }
+  const int nt0 = n0 / 16;
   const int nst = a.K / KB;
-  u4 ra[NA][2], rb0, rb1;
+  u4 ra[NA][2], rb[2];
   auto gload = [&](int s) {
     const size_t k = (size_t)s * KB;
 #pragma unroll
@@ -318,8 +334,11 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
       ra[p][0] = aok ? ld16(ap + (size_t)p * a.ldx + k) : zero16();
       ra[p][1] = aok ? ld16(ap + (size_t)p * a.ldx + k + EPL) : zero16();
     }
-    rb0 = bok ? ld16_stream(bp + k) : zero16();
-    rb1 = bok ? ld16_stream(bp + k + EPL) : zero16();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const size_t blk = (size_t)(nt0 + (brow[q] >> 4)) * nfr + s;
+      rb[q] = bok[q] ? ld16_stream(W + (blk * 64 + bidx[q]) * EPL) : zero16();
+    }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
@@ -327,8 +346,8 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
       sA[buf][p][lr * LDR + lc] = ra[p][0];
       sA[buf][p][lr * LDR + lc + 1] = ra[p][1];
     }
-    sB[buf][lr * LDR + lc] = rb0;
-    sB[buf][lr * LDR + lc + 1] = rb1;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) sB[buf][brow[q] * LDR + bg[q]] = rb[q];
   };
   f4 acc[4][4];
 #pragma unroll
@@ -359,23 +378,40 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int nb = n0 + wn * 64 + 32 * p;
-      if (nb >= a.N) continue;
+    for (int j = 0; j < 4; ++j) {
+      const int nb = n0 + wn * 64 + 16 * j;
+      if (nb >= a.N) continue;  // uniform per wave
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm * 64 + i * 16 + 4 * g + r;
-        if (m < a.M) epi_pair<T, EPI>(a, m, nb, r16, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
+        epi_tile<T, EPI>(a, m, m < a.M, nb, r16, acc[i][j][r]);
       }
     }
 }
 
 // ------------------------------------------------------------------------ launch
-template <typename T, int MT, int EPI>
+// column tiles of a skinny launch: 32-column tiles while they already give
+// enough workgroups, else 16-column tiles
+int skinny_tiles(int N) { return (N / 32 >= 512) ? N / 32 : N / 16; }
+
+template <typename T, int MT, int TN, int EPI>
 static void run_skinny(const GemmArgs& a, int nsplit, int tag, Stream s) {
-  dim3 grid(a.N / 32, nsplit);
-  if (tag) hipLaunchKernelGGL((k_gemm_skinny<T, MT, EPI, 1>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((k_gemm_skinny<T, MT, EPI, 0>), grid, dim3(256), 0, s, a);
+  dim3 grid(a.N / (16 * TN), nsplit);
+  if constexpr (EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_SWIGLU) {
+    if (!tag) {
+      hipLaunchKernelGGL((k_gemm_skinny<T, MT, TN, EPI, 0>), grid, dim3(256), 0, s, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((k_gemm_skinny<T, MT, TN, EPI, 1>), grid, dim3(256), 0, s, a);
+}
+
+template <typename T, int TN, int EPI>
+static void run_skinny_mt(const GemmArgs& a, int nsplit, int tag, Stream s) {
+  const int mt = (a.M + 15) / 16;
+  if (mt == 1) run_skinny<T, 1, TN, EPI>(a, nsplit, tag, s);
+  else if (mt == 2) run_skinny<T, 2, TN, EPI>(a, nsplit, tag, s);
+  else run_skinny<T, 4, TN, EPI>(a, nsplit, tag, s);
 }
 
 template <typename T, int EPI>
@@ -393,8 +429,9 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
       return 0;
     }
   }
-  const int ntiles = a.N / 32;
   const int nfr = a.K / KB;
+  const int ntiles = skinny_tiles(a.N);
+  const int TN = a.N / (16 * ntiles);
   int nsplit = 1;
   if (EPI != EPI_ARGMAX && EPI != EPI_SWIGLU && max_split > 1) {
     // about 1024 workgroups, at least four fragments per wave
@@ -404,10 +441,8 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
   }
   a.nsplit = nsplit;
   *nsplit_out = nsplit;
-  const int mt = (a.M + 15) / 16;
-  if (mt == 1) run_skinny<T, 1, EPI>(a, nsplit, tag, s);
-  else if (mt == 2) run_skinny<T, 2, EPI>(a, nsplit, tag, s);
-  else run_skinny<T, 4, EPI>(a, nsplit, tag, s);
+  if (TN == 2) run_skinny_mt<T, 2, EPI>(a, nsplit, tag, s);
+  else run_skinny_mt<T, 1, EPI>(a, nsplit, tag, s);
   return 0;
 }
 
@@ -433,6 +468,7 @@ int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, 
 }
 
 int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s) {
+  // ntiles: argmax partials written per row by the LM-head launch
   hipLaunchKernelGGL(k_decide, dim3(M), dim3(256), 0, s, d, ntiles, M);
   return 0;
 }

@@ -44,7 +44,7 @@ struct MicroPrepArgs {
 };
 
 struct GenArgs {
-  void* dst; int rows, cols; long long row_off; int interleave; uint64_t key;
+  void* dst; int rows, cols; long long row_off; int interleave; int tiled; uint64_t key;
 };
 
 void launch_macro_begin(int dtype, const MacroArgs& a, Stream s);

@@ -334,8 +334,11 @@ __global__ __launch_bounds__(256) void k_gen_normal(GenArgs a) {
     const float v = (float)(nv * 0.02);
     const long long row = i / a.cols, col = i % a.cols;
     long long drow = row + a.row_off;
-    if (a.interleave) drow = 32 * (row / 16) + (row % 16) + (a.interleave == 2 ? 16 : 0) + a.row_off;
-    ((T*)a.dst)[drow * a.cols + col] = from_f<T>(v);
+    // gate and up rows interleaved in blocks of 8: one 16-row tile holds gate and up of 8 features
+    if (a.interleave) drow = 16 * (row / 8) + (row % 8) + (a.interleave == 2 ? 8 : 0) + a.row_off;
+    const size_t dst = a.tiled ? tiled_index<T>((size_t)drow, (size_t)col, (size_t)a.cols)
+                               : (size_t)drow * a.cols + col;
+    ((T*)a.dst)[dst] = from_f<T>(v);
   }
 }
 

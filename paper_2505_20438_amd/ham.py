@@ -77,8 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_kv_stats.argtypes = [P, ctypes.POINTER(HamKvStats)]
     lib.ham_set_debug.argtypes = [P, P, SZ]
     lib.ham_steps_done.argtypes = [P]
-    lib.ham_tensor_info.argtypes = [cfgp, I32, ctypes.POINTER(SZ), ctypes.POINTER(I32), ctypes.POINTER(I32),
-                                    ctypes.POINTER(I32)]
+    lib.ham_tensor_info.argtypes = [cfgp, I32, ctypes.POINTER(SZ)] + [ctypes.POINTER(I32)] * 6
     lib.ham_profile.argtypes = [P, I32]
     lib.ham_profile_read.argtypes = [P, ctypes.POINTER(HamProfT), I32]
     lib.ham_op_attention_workspace_bytes.argtypes = [I32, I32, I32, I32]
@@ -129,11 +128,15 @@ def ham_workspace_bytes(cfg: HamConfig) -> int:
     return load_library().ham_workspace_bytes(ctypes.byref(cfg))
 
 
-def ham_tensor_info(cfg: HamConfig, tensor_id: int):
-    off, rows, cols, inter = ctypes.c_size_t(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
-    _check(load_library().ham_tensor_info(ctypes.byref(cfg), tensor_id, ctypes.byref(off), ctypes.byref(rows),
-                                          ctypes.byref(cols), ctypes.byref(inter)))
-    return off.value, rows.value, cols.value, inter.value
+def ham_tensor_info(cfg: HamConfig, tensor_id: int) -> dict:
+    off = ctypes.c_size_t()
+    v = [ctypes.c_int32() for _ in range(6)]
+    _check(load_library().ham_tensor_info(ctypes.byref(cfg), tensor_id, ctypes.byref(off),
+                                          *[ctypes.byref(x) for x in v]))
+    keys = ("rows", "cols", "row_off", "mat_rows", "interleave", "tiled")
+    d = {k: x.value for k, x in zip(keys, v)}
+    d["offset"] = off.value
+    return d
 
 
 def ham_init_weights(cfg: HamConfig, seed: int, weights, state, workspace, stream: int) -> int:
@@ -223,17 +226,23 @@ class HamRuntime:
         return ham_kv_stats(self.handle, self.batch)
 
     def tensor(self, tensor_id: int):
-        """A generated tensor as stored (row-major, rows in storage order)."""
+        """A generated tensor [rows][cols] in logical row-major order (bf16 as int16 bits)."""
         torch = self.torch
-        off, rows, cols, inter = ham_tensor_info(self.cfg, tensor_id)
+        t = ham_tensor_info(self.cfg, tensor_id)
         es = 2 if self.cfg.dtype == HAM_BF16 else 4
         dt = torch.int16 if es == 2 else torch.float32
-        span = rows * cols if not inter else 2 * rows * cols
-        flat = self.weights[off: off + span * es].view(dt)
-        if not inter:
-            return flat.view(rows, cols)
-        blocks = flat.view(rows // 16, 2, 16, cols)
-        return blocks[:, inter - 1].reshape(rows, cols)
+        R, K = t["mat_rows"], t["cols"]
+        flat = self.weights[t["offset"]: t["offset"] + R * K * es].view(dt)
+        if t["tiled"]:   # undo the fragment tiling: [tile][frag][group][row][elem] -> [tile][row][frag][group][elem]
+            epl = 16 // es
+            flat = flat.view(R // 16, K // (4 * epl), 4, 16, epl).permute(0, 3, 1, 2, 4)
+        mat = flat.reshape(R, K)
+        r = torch.arange(t["rows"], device=mat.device)
+        if t["interleave"]:
+            idx = 16 * (r // 8) + r % 8 + (8 if t["interleave"] == 2 else 0)
+        else:
+            idx = r + t["row_off"]
+        return mat[idx]
 
     def close(self):
         if self.handle:

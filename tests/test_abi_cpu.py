@@ -96,16 +96,18 @@ def test_calls_on_null_handle(lib):
 
 def test_tensor_info_layout(lib):
     cfg = config_for(TINY, 1, 8, 4)
-    seen = []
+    total = ham.ham_weights_bytes(cfg)
     ids = list(range(9)) + [16 + 8 * j + t for j in range(TINY.n_layers + TINY.micro_layers) for t in range(7)]
-    for tid in ids:
-        off, rows, cols, inter = ham.ham_tensor_info(cfg, tid)
-        assert off % 256 == 0 or tid in (3, 4, 8) or (tid >= 16 and (tid - 16) % 8 in (1, 2, 5))
-        assert off + rows * cols * 4 <= ham.ham_weights_bytes(cfg)
-        seen.append((off, rows, cols, inter))
-    assert seen[0][1:3] == (TINY.vocab, TINY.d_model)
-    wg, wu = seen[9 + 4], seen[9 + 5]
-    assert wg[0] == wu[0] and (wg[3], wu[3]) == (1, 2) and wg[1] == TINY.ffn_dim
+    info = {tid: ham.ham_tensor_info(cfg, tid) for tid in ids}
+    for tid, t in info.items():
+        assert t["offset"] % 256 == 0
+        assert t["offset"] + t["mat_rows"] * t["cols"] * 4 <= total
+        assert t["row_off"] + t["rows"] <= t["mat_rows"] or t["interleave"]
+    assert (info[0]["rows"], info[0]["cols"], info[0]["tiled"]) == (TINY.vocab, TINY.d_model, 0)
+    assert info[7]["tiled"] == 1 and info[8]["row_off"] == TINY.vocab      # stop head = extra LM-head row
+    wg, wu = info[16 + 4], info[16 + 5]
+    assert wg["offset"] == wu["offset"] and (wg["interleave"], wu["interleave"]) == (1, 2)
+    assert wg["mat_rows"] == 2 * TINY.ffn_dim
     with pytest.raises(ham.HamError):
         ham.ham_tensor_info(cfg, 12)
     with pytest.raises(ham.HamError):

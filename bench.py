@@ -30,7 +30,8 @@ HBM_PEAK_GBS = 8000.0
 PROF_NAMES = ["qkv", "o_proj", "gate_up", "down", "micro_gemm", "embed_gemm", "lm_head_k0", "lm_head_micro",
               "attn_decode"]
 DOMINANT_KERNEL = {
-    2: "k_gemm_skinny<bf16, 2, 1, EPI_SWIGLU, 0> (base-layer gate/up weight streaming, SwiGLU epilogue)",
+    # template arguments: element type, 16-row tiles, 16-column tiles per wave, epilogue (3 = SwiGLU), tag
+    "gate_up": "k_gemm_skinny<unsigned short, 1, 2, 3, 0> (base-layer gate/up weight streaming, SwiGLU epilogue)",
 }
 
 
@@ -187,8 +188,8 @@ def main() -> int:
     roofline = {"bound": "hbm", "achieved": kd["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": kd["gbs"] / HBM_PEAK_GBS, "traffic": None, "kernel": dom,
                 "bytes_per_launch": kd["bytes_per_launch"], "avg_us": kd["avg_us"]}
-    if dom == "gate_up" and s.dtype == BF16 and B <= 16:
-        roofline["kernel_name"] = DOMINANT_KERNEL[2]
+    if dom == "gate_up" and s.dtype == BF16 and B <= 16 and s.ffn_dim * 2 // 32 >= 512:
+        roofline["kernel_name"] = DOMINANT_KERNEL["gate_up"]
 
     out = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,

@@ -81,7 +81,9 @@ typedef struct ham_kv_stats_t {
   int32_t groups;        /* groups emitted, including the one from prefill */
   int32_t done;          /* 1 once the token budget is spent */
   int32_t len_hist[5];   /* groups of length 0..4 */
-  int32_t device_error;  /* nonzero if a device-side bounds check tripped */
+  int32_t device_error;  /* nonzero if a device-side check tripped (bit mask): 1 RoPE position or
+                          * KV slot out of range, 2 prompt token id out of range, 4 teacher token
+                          * out of range, 8 new KV slot inconsistent with the cache length */
 } ham_kv_stats_t;
 
 typedef struct ham_model ham_model;

@@ -67,7 +67,7 @@ struct Layout {
   size_t Kc, VTc, kv_layer, seq, st_bytes;
   // workspace
   size_t x, xp, xn, qkv, q, ao, act, part, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
-      Kloc, VTloc, loc_layer, ws_bytes;
+      rope_cs, Kloc, VTloc, loc_layer, ws_bytes;
 };
 
 const char* check_cfg(const ham_config* c) {
@@ -160,6 +160,7 @@ Layout make_layout(const ham_config* c) {
   y.emb_in = take((size_t)5 * y.B * y.d * 4);
   y.emb_o = take((size_t)y.B * y.HD * 4);
   y.emb_y = take((size_t)y.B * y.d * 4);
+  y.rope_cs = take((size_t)y.B * y.hd * 4);
   y.loc_layer = al((size_t)y.B * y.Hk * LOCAL_SLOTS * y.hd * es);
   y.Kloc = take(y.loc_layer * y.M);
   y.VTloc = take(y.loc_layer * y.M);
@@ -271,46 +272,15 @@ void norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* 
   pend = Pending{};
 }
 
-// one transformer layer (base layer j < L, micro layer j >= L) over R rows.
-// On entry `pend` may hold the previous layer's down-projection partials (folded
-// into x by the first norm, which also copies the updated rows to ctx_prev); on
-// exit it holds this layer's, if split.
-int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefill, void* Kc, void* VTc,
-              long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
-              float* ctx_prev, int ldctx, int kv_visible) {
+// The rest of a layer after attention: o-projection into the residual, second
+// norm, gate/up with the SwiGLU epilogue, down-projection into the residual.
+template <typename GK>
+int layer_tail(ham_model* m, int j, int R, float* x, int split, const int* gate, int gate_n, Pending& pend,
+               const GK& gk) {
   const Layout& y = m->y;
-  const int dt = dtype_of(m);
-  hipStream_t s = m->s;
-  const bool base = !prefill && j < y.L;
-  const auto gk = [&](int kind) { return prefill ? -1 : (base ? kind : HAM_PROF_MICRO); };
-  const int split = prefill ? 1 : MAX_GEMM_SPLIT;
   int ns = 1;
-  norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
-
   GemmArgs ga{};
-  ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n;
-  ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = R;
-  ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
-  if (gemm_p(m, EPI_F32, ga, split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
-
-  RopeArgs ra{};
-  ra.qkv = m->WS<float>(y.qkv); ra.ldqkv = y.QKV; ra.R = R; ra.q = m->WS<char>(y.q); ra.ldq = y.HD;
-  ra.part = ns > 1 ? m->WS<float>(y.part) : nullptr; ra.nsplit = ns;
-  ra.K = Kc; ra.VT = VTc; ra.sb = sb; ra.sh = sh; ra.S = S; ra.H = y.H; ra.Hkv = y.Hk; ra.hd = y.hd;
-  ra.cos_t = m->W<float>(y.cos_t); ra.sin_t = m->W<float>(y.sin_t); ra.max_pos = y.max_pos; ra.rm = rm;
-  ra.gate = gate; ra.gate_n = gate_n;
-  launch_rope_append(dt, ra, s);
-
-  AttnArgs aa{};
-  aa.q = m->WS<char>(y.q); aa.ldq = y.HD; aa.K = Kc; aa.VT = VTc; aa.sb = sb; aa.sh = sh; aa.S = S;
-  aa.H = y.H; aa.Hkv = y.Hk; aa.hd = y.hd; aa.R = R; aa.nsplit = attn_split; aa.o = m->WS<char>(y.ao);
-  aa.ldo = y.HD; aa.part = m->WS<float>(y.apart); aa.rm = rm;
-  aa.gate = gate; aa.gate_n = gate_n;
-  m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
-  const int arc = prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s);
-  m->pend();
-  if (arc != 0) return fail(HAM_EINVAL, "attention shape");
-
+  ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n; ga.M = R;
   ga.W = m->W<char>(y.Wo[j]); ga.N = y.d; ga.K = y.HD; ga.X = m->WS<char>(y.ao); ga.ldx = y.HD;
   ga.out = x; ga.ldo = y.d;
   if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_O), &ns)) return fail(HAM_EINVAL, "o-proj gemm shape");
@@ -327,6 +297,90 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefi
   if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_DOWN), &ns)) return fail(HAM_EINVAL, "down gemm shape");
   if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
   return HAM_OK;
+}
+
+// Fused decode step of a layer (rows of mode DECODE or MICROK): where the RoPE
+// factors of each row are, and the bound on the cached slots of every row.
+struct StepAttn {
+  const float* cos_p;
+  const float* sin_p;
+  long long cs_stride;
+  int kv_cap;
+};
+
+// slot splits of the fused step: none while each wave holds at most four chunks
+// of key blocks; otherwise about two chunks per wave
+int attn_step_splits(int dtype, int Hk, int hd, int kv_cap) {
+  (void)Hk;
+  const int kb = dtype == HAM_BF16 ? 32 : 16;
+  const int blocks = (kv_cap + kb - 1) / kb;
+  const int chunk = 8 * (256 / hd);  // key blocks one workgroup holds in flight
+  if (blocks <= 4 * chunk) return 1;
+  return std::min(MAX_ATTN_SPLIT, (blocks + 2 * chunk - 1) / (2 * chunk));
+}
+
+// one transformer layer (base layer j < L, micro layer j >= L) over R rows.
+// On entry `pend` may hold the previous layer's down-projection partials (folded
+// into x by the first norm, which also copies the updated rows to ctx_prev); on
+// exit it holds this layer's, if split.
+int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefill, void* Kc, void* VTc,
+              long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
+              float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step) {
+  const Layout& y = m->y;
+  const int dt = dtype_of(m);
+  hipStream_t s = m->s;
+  const bool base = !prefill && j < y.L;
+  const auto gk = [&](int kind) { return prefill ? -1 : (base ? kind : HAM_PROF_MICRO); };
+  // Base layers run for every sequence of the batch (finished rows compute values that
+  // nothing reads; their KV append and decisions are skipped per row), so they carry no
+  // gate: a gate costs a dependent memory round trip before any other load.
+  if (base) {
+    gate = nullptr;
+    gate_n = 0;
+  }
+  const int split = prefill ? 1 : MAX_GEMM_SPLIT;
+  int ns = 1;
+  norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
+
+  GemmArgs ga{};
+  ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n;
+  ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = R;
+  ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
+  const int qkv_split = step ? std::min(split, attn_step_max_qkv_split()) : split;
+  if (gemm_p(m, EPI_F32, ga, qkv_split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
+
+  if (step) {
+    AttnStepArgs sa{};
+    sa.qkv = m->WS<float>(y.qkv); sa.part = ns > 1 ? m->WS<float>(y.part) : nullptr; sa.nsplit_qkv = ns;
+    sa.pM = R; sa.ldqkv = y.QKV;
+    sa.cos_p = step->cos_p; sa.sin_p = step->sin_p; sa.cs_stride = step->cs_stride;
+    sa.K = Kc; sa.VT = VTc; sa.sb = sb; sa.sh = sh; sa.S = S;
+    sa.H = y.H; sa.Hkv = y.Hk; sa.hd = y.hd; sa.R = R; sa.nsplit = attn_split; sa.kv_cap = step->kv_cap;
+    sa.o = m->WS<char>(y.ao); sa.ldo = y.HD; sa.part_out = m->WS<float>(y.apart); sa.rm = rm;
+    m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
+    const int arc = launch_attn_step(dt, sa, s);
+    m->pend();
+    if (arc != 0) return fail(HAM_EINVAL, "attention step shape");
+    return layer_tail(m, j, R, x, split, gate, gate_n, pend, gk);
+  }
+
+  RopeArgs ra{};
+  ra.qkv = m->WS<float>(y.qkv); ra.ldqkv = y.QKV; ra.R = R; ra.q = m->WS<char>(y.q); ra.ldq = y.HD;
+  ra.part = ns > 1 ? m->WS<float>(y.part) : nullptr; ra.nsplit = ns;
+  ra.K = Kc; ra.VT = VTc; ra.sb = sb; ra.sh = sh; ra.S = S; ra.H = y.H; ra.Hkv = y.Hk; ra.hd = y.hd;
+  ra.cos_t = m->W<float>(y.cos_t); ra.sin_t = m->W<float>(y.sin_t); ra.max_pos = y.max_pos; ra.rm = rm;
+  ra.gate = gate; ra.gate_n = gate_n;
+  launch_rope_append(dt, ra, s);
+
+  AttnArgs aa{};
+  aa.q = m->WS<char>(y.q); aa.ldq = y.HD; aa.K = Kc; aa.VT = VTc; aa.sb = sb; aa.sh = sh; aa.S = S;
+  aa.H = y.H; aa.Hkv = y.Hk; aa.hd = y.hd; aa.R = R; aa.nsplit = attn_split; aa.o = m->WS<char>(y.ao);
+  aa.ldo = y.HD; aa.part = m->WS<float>(y.apart); aa.rm = rm;  // rows gate themselves (row map)
+  m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
+  const int arc = prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s);
+  m->pend();
+  if (arc != 0) return fail(HAM_EINVAL, "attention shape");
+  return layer_tail(m, j, R, x, split, gate, gate_n, pend, gk);
 }
 
 // final norm of one row per sequence (folding in pending partials, capturing the
@@ -373,10 +427,14 @@ int decode_tail(ham_model* m, Pending& pend, float* ctx_last, int* out_tokens, i
     rm.mode = k == 1 ? ROWS_MICRO1 : ROWS_MICROK; rm.C = y.C; rm.k = k; rm.st = m->sp;
     const int R = k == 1 ? B * (y.C + 1) : B;
     Pending mp_pend;
+    // micro step k >= 2: one new local slot per sequence at local position C + k - 1
+    const int lpos = y.C + k - 1, half = y.hd / 2;
+    const StepAttn lstep{m->W<float>(y.cos_t) + (size_t)lpos * half, m->W<float>(y.sin_t) + (size_t)lpos * half, 0,
+                         lpos};
     for (int mj = 0; mj < y.M; ++mj) {
       rc = run_layer(m, y.L + mj, R, rm, x, false, m->WS<char>(y.Kloc + mj * y.loc_layer),
                      m->WS<char>(y.VTloc + mj * y.loc_layer), lsb, lsh, LOCAL_SLOTS, 1, m->sp.active, B, mp_pend,
-                     nullptr, 0, k == 1 ? B * (y.C + 1) * (y.C + 2) / 2 : B * (y.C + k));
+                     nullptr, 0, k == 1 ? B * (y.C + 1) * (y.C + 2) / 2 : B * (y.C + k), k == 1 ? nullptr : &lstep);
       if (rc) return rc;
     }
     rc = run_decision(m, k, x, k == 1 ? y.C + 1 : 1, k == 1 ? y.C : 0, m->W<float>(y.gmf), mp_pend, nullptr,
@@ -397,7 +455,6 @@ int attn_splits_for(int dtype, int R, int Hk, int kv_max) {
   const int most = std::max(1, blocks / (8 * 2));  // at least 2 blocks per wave
   return std::max(1, std::min(std::min(want, most), MAX_ATTN_SPLIT));
 }
-int attn_splits(const ham_model* m, int R, int kv_max) { return attn_splits_for(m->cfg.dtype, R, m->y.Hk, kv_max); }
 
 size_t attn_part_bytes(int R, int H, int Hk, int hd) {
   return (size_t)R * Hk * MAX_ATTN_SPLIT * (H / Hk) * (hd + 2) * 4;
@@ -575,7 +632,7 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
       for (int l = 0; l < y.L; ++l) {
         Pending none;
         int rc = run_layer(m, l, R, rm, xp, true, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer,
-                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0);
+                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0, nullptr);
         if (rc) return rc;
         if (last)
           for (int c = 0; c < y.C; ++c)
@@ -611,6 +668,8 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   ma.st = m->sp; ma.B = B; ma.d = y.d; ma.G = y.G; ma.E = m->W<char>(y.E); ma.P = m->W<char>(y.Pe); ma.x = x;
   ma.ldx = y.d; ma.emb_in = m->WS<char>(y.emb_in); ma.forced_in = d_forced_lens; ma.teacher_in = d_teacher;
   ma.out_tokens = d_out_tokens; ma.out_lens = d_out_lens;
+  ma.cos_t = m->W<float>(y.cos_t); ma.sin_t = m->W<float>(y.sin_t); ma.max_pos = y.max_pos; ma.hd = y.hd;
+  ma.rope_cs = m->WS<float>(y.rope_cs);
   launch_macro_begin(dt, ma, s);
 
   // compositional embedder (Sec. 3.2), skipped on device unless some group has > 1 token
@@ -644,15 +703,16 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   RowMap rm{};
   rm.mode = ROWS_DECODE; rm.st = m->sp;
   const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
-  const int kv_max = m->prompt_len + m->steps_done + 1;
-  const int nsplit = attn_splits(m, B, kv_max);
-  m->kv_visible = B * kv_max;  // every running sequence holds the same count at this step (upper bound)
+  const int kv_max = m->prompt_len + m->steps_done + 1;  // every sequence holds at most this many slots now
+  const int nsplit = attn_step_splits(dt, y.Hk, y.hd, kv_max - 1);
+  m->kv_visible = B * kv_max;
+  const StepAttn bstep{m->WS<float>(y.rope_cs), m->WS<float>(y.rope_cs) + y.hd / 2, y.hd, kv_max - 1};
   float* ctx = m->WS<float>(y.ctx);
   Pending pend;
   float* ctx_prev = nullptr;  // context slot of the previous layer's output, captured by the next norm
   for (int l = 0; l < y.L; ++l) {
     int rc = run_layer(m, l, B, rm, x, false, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer, sb,
-                       sh, y.S, nsplit, m->sp.step_on, B, pend, ctx_prev, y.C * y.d, m->kv_visible);
+                       sh, y.S, nsplit, m->sp.step_on, B, pend, ctx_prev, y.C * y.d, m->kv_visible, &bstep);
     if (rc) return rc;
     ctx_prev = nullptr;
     for (int c = 0; c < y.C; ++c)

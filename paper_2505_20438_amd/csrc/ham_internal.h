@@ -80,6 +80,19 @@ struct AttnArgs {
   const int* gate; int gate_n;
 };
 
+// Fused decode step (rows of mode DECODE or MICROK): projection finish, RoPE,
+// KV append of the new slot and attention over the cache plus that slot.
+struct AttnStepArgs {
+  const float* qkv; const float* part; int nsplit_qkv, pM, ldqkv;  // projection [R][ldqkv] or partials [ns][pM][ldqkv]
+  const float* cos_p; const float* sin_p; long long cs_stride;     // RoPE factors of row r at +r*cs_stride (hd/2 each)
+  void* K; void* VT; long long sb, sh; int S;                      // caches as in AttnArgs; row r is sequence r
+  int H, Hkv, hd, R, nsplit;
+  int kv_cap;                      // bound on the cached slots of every row (new slot excluded)
+  void* o; int ldo;                // o [R][H*hd] (storage type)
+  float* part_out;                 // split partials [R][Hkv][nsplit][grp][hd+2]
+  RowMap rm;
+};
+
 // ---------------------------------------------------------------- launchers
 typedef hipStream_t Stream;
 // tag 0: base-layer launch (distinct kernel name in profiles), 1: any other.
@@ -90,6 +103,8 @@ int skinny_tiles(int N);  // column tiles (argmax partials per row) of a skinny 
 int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s);
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s);
 int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s);
+int launch_attn_step(int dtype, const AttnStepArgs& a, Stream s);
+int attn_step_max_qkv_split();  // most split-K partials of the projection the step kernel sums
 
 struct RopeArgs {
   const float* qkv; int ldqkv, R;  // [R][(H+2Hkv)hd] fp32 projections

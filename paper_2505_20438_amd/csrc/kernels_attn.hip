@@ -75,15 +75,35 @@ __device__ __forceinline__ void kv_load(KVBlock<T, HD>& blk, const T* Kb, const 
   for (int dt = 0; dt < B::ND; ++dt) blk.v[dt] = ld16_stream(vp + (size_t)dt * 16 * S);
 }
 
+// Keep the first `keep` elements of a lane fragment, zero the rest.
+template <typename T> __device__ __forceinline__ void keep_first(u4& v, int keep);
+template <> __device__ __forceinline__ void keep_first<bf16>(u4& v, int keep) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (e >= keep) v[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+}
+template <> __device__ __forceinline__ void keep_first<float>(u4& v, int keep) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (e >= keep) v[e] = 0u;
+}
+
 // Scores of the 16 operand rows against the block (lane: row r16, slots
-// base + g*KB/4 + e), masked at `limit`, then the online-softmax update of
-// (m, l, o) and the P.V product.
+// base + g*KB/4 + e), masked at `limit` (the lane's row), then the
+// online-softmax update of (m, l, o) and the P.V product.  Values of slots at
+// or past `vlimit` (the same for every lane) are zeroed first, so whatever a
+// slot past the end holds cannot reach the output.
 template <typename T, int HD>
-__device__ __forceinline__ void attn_block(const KVBlock<T, HD>& blk, int base, int limit, const u4* qf,
+__device__ __forceinline__ void attn_block(KVBlock<T, HD>& blk, int base, int limit, int vlimit, const u4* qf,
                                            const u4* ql, float scale, float& mrun, float& lrun, f4* o) {
   using B = KVBlock<T, HD>;
-  constexpr int KB = B::KB, ND = B::ND, TT = B::TT;
+  constexpr int KB = B::KB, ND = B::ND, TT = B::TT, EPL = Frag<T>::EPL;
   const int lane = threadIdx.x & 63, g = lane >> 4;
+  if (base + KB > vlimit) {
+    const int keep = min(max(vlimit - (base + g * EPL), 0), EPL);
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) keep_first<T>(blk.v[dt], keep);
+  }
   float sc[KB / 4];
 #pragma unroll
   for (int t = 0; t < TT; ++t) {
@@ -129,35 +149,107 @@ __device__ __forceinline__ void attn_block(const KVBlock<T, HD>& blk, int base, 
   }
 }
 
-// blocks [b0, b1) of KB slots from s0, limit `limit`; block i+1 loads while i computes
+// key blocks a wave keeps in flight at once: 8 KB (head dim 64) or 16 KB (128) of K and V each
+template <int HD> struct AttnChunk { static constexpr int NB = 256 / HD; };
+
+// Key blocks [b0, b1) of KB slots from slot0, masked at `limit` / `vlimit`.
+// The blocks go in chunks of NB whose loads are all issued before any of them
+// is used, so a chunk costs one memory round trip.
 template <typename T, int HD>
-__device__ __forceinline__ void attn_range(const T* Kb, const T* Vb, int S, int s0, int b0, int b1, int limit,
-                                           const u4* qf, const u4* ql, float scale, float& mrun, float& lrun,
-                                           f4* o) {
-  constexpr int KB = Frag<T>::KB;
-  if (b0 >= b1) return;
-  KVBlock<T, HD> cur, nxt;
-  kv_load<T, HD>(cur, Kb, Vb, S, s0 + b0 * KB);
-  for (int bk = b0; bk < b1; ++bk) {
-    const bool more = bk + 1 < b1;
-    if (more) kv_load<T, HD>(nxt, Kb, Vb, S, s0 + (bk + 1) * KB);
-    attn_block<T, HD>(cur, s0 + bk * KB, limit, qf, ql, scale, mrun, lrun, o);
-    if (more) cur = nxt;
+__device__ __forceinline__ void attn_blocks(const T* Kb, const T* Vb, int S, int slot0, int b0, int b1, int limit,
+                                            int vlimit, const u4* qf, const u4* ql, float scale, float& mrun,
+                                            float& lrun, f4* o) {
+  constexpr int KB = Frag<T>::KB, NB = AttnChunk<HD>::NB;
+  for (int c = b0; c < b1; c += NB) {
+    KVBlock<T, HD> blk[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      if (c + i < b1) kv_load<T, HD>(blk[i], Kb, Vb, S, slot0 + (c + i) * KB);
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      if (c + i < b1) attn_block<T, HD>(blk[i], slot0 + (c + i) * KB, limit, vlimit, qf, ql, scale, mrun, lrun, o);
   }
 }
 
-// One workgroup per (query row, kv head, slot split); its NW waves take
-// consecutive key blocks of the split's slot range and merge their (max, sum,
-// output) through LDS in wave order.  With one split the workgroup writes the
-// final output; otherwise it writes the split's partial for k_attn_combine.
 constexpr int ATTN_NW = 8;
 
+// Shared state of one (row, kv head, split) workgroup: per wave the softmax
+// max, sum and unnormalised output rows of its q-heads, plus an optional extra
+// one-slot state (score, value) merged after the waves.
+template <int HD>
+struct AttnLds {
+  float O[ATTN_NW][4][HD];
+  float M[ATTN_NW][16], L[ATTN_NW][16];
+  float xs[4];      // extra slot: scaled score per q-head
+  float xv[HD];     // extra slot: value
+};
+
+template <typename T, int HD>
+__device__ __forceinline__ void attn_publish(AttnLds<HD>& sh, int grp, float mrun, float lrun, const f4* o) {
+  constexpr int ND = HD / 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
+  if (g == 0) {
+    sh.M[w][r16] = mrun;
+    sh.L[w][r16] = lrun;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = 4 * g + i;  // rows 4g+i of the output live in lane group g
+    if (j < grp) {
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) sh.O[w][j][dt * 16 + r16] = o[dt][i];
+    }
+  }
+}
+
+// After a barrier: merge the waves in order (then the extra slot, if any); each
+// thread owns (q-head j, column d) pairs.  One split: normalised output; else
+// the split's (O, max, sum) record for k_attn_combine.
+template <typename T, int HD>
+__device__ __forceinline__ void attn_merge_store(const AttnLds<HD>& sh, bool extra, int grp, int r, int kvh,
+                                                 int split, int nsplit, int Hkv, void* out, int ldo, float* part) {
+  const size_t rec = HD + 2;
+  float* pb = part + (((size_t)r * Hkv + kvh) * nsplit) * grp * rec;
+  for (int t = threadIdx.x; t < grp * HD; t += 64 * ATTN_NW) {
+    const int j = t / HD, d = t % HD;
+    float M = extra ? sh.xs[j] : -INFINITY;
+#pragma unroll
+    for (int q = 0; q < ATTN_NW; ++q) M = fmaxf(M, sh.M[q][j]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < ATTN_NW; ++q) {
+        const float wgt = sh.M[q][j] == -INFINITY ? 0.f : __expf(sh.M[q][j] - M);
+        L += wgt * sh.L[q][j];
+        O += wgt * sh.O[q][j][d];
+      }
+      if (extra) {
+        const float wgt = __expf(sh.xs[j] - M);
+        L += wgt;
+        O += wgt * sh.xv[d];
+      }
+    }
+    if (nsplit == 1) {
+      Act<T>::put(out, r, ldo, (kvh * grp + j) * HD + d, L > 0.f ? O / L : 0.f);
+    } else {
+      float* pj = pb + ((size_t)split * grp + j) * rec;
+      pj[d] = O;
+      if (d == 0) {
+        pj[HD] = M;
+        pj[HD + 1] = L;
+      }
+    }
+  }
+}
+
+// One workgroup per (query row, kv head, slot split) over a cache that already
+// holds every visible slot (the attention op, the micro decoder's first step);
+// its waves take consecutive key blocks of the split's slot range.
 template <typename T, int HD>
 __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_decode(AttnArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16;
-  __shared__ float sO[ATTN_NW][4][HD];   // per wave: output rows of up to 4 q-heads (grp <= 4 here)
-  __shared__ float sM[ATTN_NW][16], sL[ATTN_NW][16];
+  __shared__ AttnLds<HD> sh;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
   const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
   const int grp = a.H / a.Hkv;
@@ -167,7 +259,6 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_decode(AttnArgs a) {
   chunk = (chunk + KB - 1) / KB * KB;
   const int s0 = split * chunk;
   const int s1 = min(nval, s0 + chunk);
-  // this wave's key blocks: a contiguous share of the split's blocks
   const int nblk = s1 > s0 ? (s1 - s0 + KB - 1) / KB : 0;
   const int b0 = w * nblk / ATTN_NW, b1 = (w + 1) * nblk / ATTN_NW;
   const T* Kb = (const T*)a.K + ri.b * a.sb + kvh * a.sh;
@@ -185,50 +276,177 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_decode(AttnArgs a) {
   for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
-  attn_range<T, HD>(Kb, Vb, a.S, s0, b0, b1, s1, qf, ql, scale, mrun, lrun, o);
-
-  // publish this wave's state; rows 4g+i of the output live in lane group g
-  if (g == 0) {
-    sM[w][r16] = mrun;
-    sL[w][r16] = lrun;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int j = 4 * g + i;
-    if (j < grp) {
-#pragma unroll
-      for (int dt = 0; dt < ND; ++dt) sO[w][j][dt * 16 + r16] = o[dt][i];
-    }
-  }
+  attn_blocks<T, HD>(Kb, Vb, a.S, s0, b0, b1, s1, s1, qf, ql, scale, mrun, lrun, o);
+  attn_publish<T, HD>(sh, grp, mrun, lrun, o);
   __syncthreads();
-  // merge the waves in order: each thread owns (head j, column d) pairs
-  const size_t rec = HD + 2;
-  float* pb = a.part + (((size_t)r * a.Hkv + kvh) * a.nsplit) * grp * rec;
-  for (int t = threadIdx.x; t < grp * HD; t += 64 * ATTN_NW) {
-    const int j = t / HD, d = t % HD;
-    float M = -INFINITY;
+  attn_merge_store<T, HD>(sh, false, grp, r, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part);
+}
+
+// ---------------------------------------------------------------- fused decode step
+// One decode row per sequence whose newest slot is produced by this step (the
+// base model's fused input, or micro step k >= 2): finishes the q/k/v
+// projection (sum of the split-K partials in split order), applies rotate-half
+// RoPE to q and k, appends k and v to the cache (split 0 only), and attends
+// over the cached slots plus the new one, which enters from registers as an
+// extra one-slot softmax state, so no workgroup reads a slot written in the
+// same launch.  Key blocks are partitioned statically over the host's bound on
+// the cached slots, so their loads need nothing from the per-row state.
+//
+// RoPE in the fragment layout: lane (r16, g) holds elements f*KB + g*EPL + e of
+// fragment f; the rotate-half partner of fragment f < NF/2 is fragment
+// f + NF/2 at the same (g, e), so every rotation stays inside one lane.
+constexpr int ATTN_STEP_MAXS = 8;  // split-K partials of the projection summed by the step kernel
+
+template <typename T, int HD>
+__global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16, NB = AttnChunk<HD>::NB;
+  constexpr int MAXS = ATTN_STEP_MAXS;
+  __shared__ AttnLds<HD> sh;
+  __shared__ float sraw[6 * HD];  // summed projection: q-heads (grp*HD) | k (HD) | v (HD)
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
+  const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
+  const int grp = a.H / a.Hkv;
+  const T* Kb = (const T*)a.K + (size_t)r * a.sb + kvh * a.sh;  // decode rows: row r is sequence r
+  const T* Vb = (const T*)a.VT + (size_t)r * a.sb + kvh * a.sh;
+  // this wave's key blocks: static share of the split's blocks of [0, kv_cap)
+  const int nblk_all = (a.kv_cap + KB - 1) / KB;
+  const int per = (nblk_all + a.nsplit - 1) / a.nsplit;
+  const int sb0 = min(nblk_all, split * per), sb1 = min(nblk_all, sb0 + per);
+  const int b0 = sb0 + w * (sb1 - sb0) / ATTN_NW, b1 = sb0 + (w + 1) * (sb1 - sb0) / ATTN_NW;
+  // first chunk of keys in flight before anything else
+  KVBlock<T, HD> blk[NB];
 #pragma unroll
-    for (int q = 0; q < ATTN_NW; ++q) M = fmaxf(M, sM[q][j]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
+  for (int i = 0; i < NB; ++i)
+    if (b0 + i < b1) kv_load<T, HD>(blk[i], Kb, Vb, a.S, (b0 + i) * KB);
+  const RowInfo ri = row_info(a.rm, r);
+  // the projection values of this kv head: one 4-float chunk per thread, all splits
+  const int nch = (grp + 2) * HD / 4;
+  const int ns = a.part ? a.nsplit_qkv : 1;
+  const float* src = a.part ? a.part : a.qkv;
+  const size_t sstride = (size_t)a.pM * a.ldqkv;
+  if (threadIdx.x < nch) {
+    const int c = threadIdx.x * 4;
+    int col;
+    if (c < grp * HD) col = kvh * grp * HD + c;
+    else if (c < (grp + 1) * HD) col = a.H * HD + kvh * HD + (c - grp * HD);
+    else col = (a.H + a.Hkv) * HD + kvh * HD + (c - (grp + 1) * HD);
+    const float* p = src + (size_t)r * a.ldqkv + col;
+    f4 t[MAXS];
 #pragma unroll
-      for (int q = 0; q < ATTN_NW; ++q) {
-        const float wgt = sM[q][j] == -INFINITY ? 0.f : __expf(sM[q][j] - M);
-        L += wgt * sL[q][j];
-        O += wgt * sO[q][j][d];
+    for (int s = 0; s < MAXS; ++s)
+      if (s < ns) t[s] = *reinterpret_cast<const f4*>(p + (size_t)s * sstride);
+    f4 acc = t[0];
+#pragma unroll
+    for (int s = 1; s < MAXS; ++s)
+      if (s < ns) acc += t[s];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sraw[c + e] = acc[e];
+  }
+  // RoPE factors of this row: elements i = f*KB + g*EPL + e, f < NF/2
+  const float* cp = a.cos_p + (size_t)r * a.cs_stride;
+  const float* sp = a.sin_p + (size_t)r * a.cs_stride;
+  float cs[NF / 2][EPL], sn[NF / 2][EPL];
+#pragma unroll
+  for (int f = 0; f < NF / 2; ++f)
+#pragma unroll
+    for (int e4 = 0; e4 < EPL; e4 += 4) {
+      const f4 cv = *reinterpret_cast<const f4*>(cp + f * KB + g * EPL + e4);
+      const f4 sv = *reinterpret_cast<const f4*>(sp + f * KB + g * EPL + e4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        cs[f][e4 + e] = cv[e];
+        sn[f][e4 + e] = sv[e];
       }
     }
-    if (a.nsplit == 1) {
-      Act<T>::put(a.o, r, a.ldo, (kvh * grp + j) * HD + d, L > 0.f ? O / L : 0.f);
-    } else {
-      float* pj = pb + ((size_t)split * grp + j) * rec;
-      pj[d] = O;
-      if (d == 0) {
-        pj[HD] = M;
-        pj[HD + 1] = L;
+  __syncthreads();
+  // rotated q (this lane's q-head r16) and k, in fragment order
+  float qv[NF][EPL], kv[NF][EPL];
+  const int qh = min(r16, grp - 1);
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      qv[f][e] = sraw[qh * HD + f * KB + g * EPL + e];
+      kv[f][e] = sraw[grp * HD + f * KB + g * EPL + e];
+    }
+#pragma unroll
+  for (int f = 0; f < NF / 2; ++f)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const float c = cs[f][e], s = sn[f][e];
+      const float q1 = qv[f][e], q2 = qv[f + NF / 2][e];
+      qv[f][e] = q1 * c - q2 * s;
+      qv[f + NF / 2][e] = q2 * c + q1 * s;
+      const float k1 = kv[f][e], k2 = kv[f + NF / 2][e];
+      // the cache holds k in the storage type: the new slot's score uses that value
+      kv[f][e] = to_f<T>(from_f<T>(k1 * c - k2 * s));
+      kv[f + NF / 2][e] = to_f<T>(from_f<T>(k2 * c + k1 * s));
+    }
+  u4 qf[NF], ql[NF];
+  float dot = 0.f;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    if constexpr (Act<T>::SPLIT) {
+      float lo[EPL];
+      qf[f] = pack_frag_bf16(qv[f]);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        const uint32_t hw = (e & 1) ? (qf[f][e >> 1] >> 16) : (qf[f][e >> 1] & 0xFFFFu);
+        lo[e] = qv[f][e] - bf2f((bf16)hw);
       }
+      ql[f] = pack_frag_bf16(lo);
+    } else {
+      qf[f] = u4{__float_as_uint(qv[f][0]), __float_as_uint(qv[f][1]), __float_as_uint(qv[f][2]),
+                 __float_as_uint(qv[f][3])};
+      ql[f] = qf[f];
+    }
+    if (r16 >= grp) {  // operand rows past the q-heads of this kv head
+      qf[f] = zero16();
+      ql[f] = zero16();
+    }
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) dot += qv[f][e] * kv[f][e];
+  }
+  dot += __shfl_xor(dot, 16, WAVE);
+  dot += __shfl_xor(dot, 32, WAVE);
+  const float scale = 1.0f / sqrtf((float)HD);
+  // the new slot: row checks, cache append (split 0), extra softmax state
+  const int cached = ri.n_valid - 1;
+  const bool slot_ok = ri.slot == cached && ri.slot >= 0 && ri.slot < a.S && cached <= a.kv_cap;
+  const bool extra = split == 0 && ri.enabled && slot_ok;
+  if (split == 0 && ri.enabled && !slot_ok && threadIdx.x == 0) atomicOr(a.rm.st.err + r, 8);
+  if (extra) {
+    if (w == 0 && g == 0 && r16 < grp) sh.xs[r16] = dot * scale;
+    if (w == 0 && r16 == 0) {
+      T* kd = (T*)a.K + (size_t)r * a.sb + kvh * a.sh + (size_t)ri.slot * HD + g * EPL;
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        u4 pk;
+        if constexpr (Act<T>::SPLIT) pk = pack_frag_bf16(kv[f]);
+        else pk = u4{__float_as_uint(kv[f][0]), __float_as_uint(kv[f][1]), __float_as_uint(kv[f][2]),
+                     __float_as_uint(kv[f][3])};
+        *reinterpret_cast<u4*>(kd + f * KB) = pk;
+      }
+    }
+    for (int d = threadIdx.x; d < HD; d += 64 * ATTN_NW) {
+      const T v = from_f<T>(sraw[(grp + 1) * HD + d]);
+      sh.xv[d] = to_f<T>(v);
+      ((T*)a.VT)[(size_t)r * a.sb + kvh * a.sh + (size_t)d * a.S + ri.slot] = v;
     }
   }
+  // cached slots [0, cached): the first chunk is in registers already
+  const int limit = (ri.enabled && slot_ok) ? cached : 0;
+  f4 o[ND];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.f;
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+    if (b0 + i < b1) attn_block<T, HD>(blk[i], (b0 + i) * KB, limit, limit, qf, ql, scale, mrun, lrun, o);
+  attn_blocks<T, HD>(Kb, Vb, a.S, 0, b0 + NB, b1, limit, limit, qf, ql, scale, mrun, lrun, o);
+  attn_publish<T, HD>(sh, grp, mrun, lrun, o);
+  __syncthreads();
+  attn_merge_store<T, HD>(sh, extra, grp, r, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part_out);
 }
 
 // Log-sum-exp combine of the splits of one (row, head), in split order.
@@ -286,7 +504,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
   // per-lane limit: the score mask uses this lane's query row (r16)
-  attn_range<T, HD>(Kb, Vb, a.S, 0, 0, (wave_end + KB - 1) / KB, limit, qf, ql, scale, mrun, lrun, o);
+  attn_blocks<T, HD>(Kb, Vb, a.S, 0, 0, (wave_end + KB - 1) / KB, limit, wave_end, qf, ql, scale, mrun, lrun, o);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * g + i;  // query row within the wave
@@ -315,6 +533,32 @@ static int prefill_t(const AttnArgs& a, Stream s) {
   else if (a.hd == 128) hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, a);
   else return -1;
   return 0;
+}
+
+template <typename T>
+static int step_t(const AttnStepArgs& a, Stream s) {
+  dim3 grid(a.nsplit, a.Hkv, a.R);
+  if (a.hd == 64) hipLaunchKernelGGL((k_attn_step<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_step<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  else return -1;
+  if (a.nsplit > 1) {
+    AttnArgs c{};
+    c.H = a.H; c.Hkv = a.Hkv; c.hd = a.hd; c.R = a.R; c.nsplit = a.nsplit; c.o = a.o; c.ldo = a.ldo;
+    c.part = a.part_out;
+    hipLaunchKernelGGL((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, c);
+  }
+  return 0;
+}
+
+int attn_step_max_qkv_split() { return ATTN_STEP_MAXS; }
+
+int launch_attn_step(int dtype, const AttnStepArgs& a, Stream s) {
+  if (a.R <= 0) return 0;
+  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 4 || a.S % 64 != 0 || a.kv_cap < 0 || a.kv_cap > a.S || a.nsplit < 1)
+    return -1;
+  if (a.part && (a.nsplit_qkv < 1 || a.nsplit_qkv > ATTN_STEP_MAXS)) return -1;
+  if (a.rm.mode != ROWS_DECODE && a.rm.mode != ROWS_MICROK) return -1;
+  return dtype == 1 ? step_t<bf16>(a, s) : step_t<float>(a, s);
 }
 
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s) {

@@ -13,6 +13,8 @@ struct MacroArgs {
   const int* forced_in;             // [B] or null
   const int* teacher_in;            // [B][4] or null
   int* out_tokens; int* out_lens;
+  const float* cos_t; const float* sin_t; int max_pos, hd;  // RoPE tables [max_pos][hd/2]
+  float* rope_cs;                   // [B][hd]: cos | sin of this step's position, per sequence
 };
 
 struct EmbedAttnArgs {

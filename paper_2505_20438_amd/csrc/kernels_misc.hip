@@ -152,7 +152,7 @@ int launch_rope_append(int dtype, const RopeArgs& a, Stream s) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
   __shared__ int tok[4];
-  __shared__ int sn, son;
+  __shared__ int sn, son, spos;
   const int b = blockIdx.x;
   const SeqPtrs& st = a.st;
   if (threadIdx.x == 0) {
@@ -188,12 +188,15 @@ __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
   if (threadIdx.x == 0) {
     st.step_on[b] = on;
     st.fused[b] = (on && n > 1) ? n : 0;
+    spos = -1;
     if (on) {
       const int p = st.pos_last[b] + n;
       st.pos_last[b] = p;
       st.cur_pos[b] = p;
       st.cur_slot[b] = st.kv_len[b];
       st.kv_len[b] += 1;
+      if (p < 0 || p >= a.max_pos) atomicOr(st.err + b, 1);
+      spos = min(max(p, 0), a.max_pos - 1);
     }
     st.forced[b] = a.forced_in ? a.forced_in[b] : a.G;
     for (int j = 0; j < 4; ++j) {
@@ -203,6 +206,15 @@ __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
     a.out_lens[b] = 0;
     st.grp_n[b] = 0;
     st.active[b] = on;
+  }
+  // RoPE factors of this step's base input, read by every layer's attention step
+  __syncthreads();
+  const int half = a.hd / 2;
+  if (spos >= 0) {
+    for (int i = threadIdx.x; i < half; i += 256) {
+      a.rope_cs[(size_t)b * a.hd + i] = a.cos_t[(size_t)spos * half + i];
+      a.rope_cs[(size_t)b * a.hd + half + i] = a.sin_t[(size_t)spos * half + i];
+    }
   }
 }
 

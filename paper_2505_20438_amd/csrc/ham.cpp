@@ -66,7 +66,7 @@ struct Layout {
   // state
   size_t Kc, VTc, kv_layer, seq, st_bytes;
   // workspace
-  size_t x, xp, xn, qkv, q, ao, act, part, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
+  size_t x, x2, xp, xn, qkv, q, ao, act, part, qpart, ssb, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
       rope_cs, Kloc, VTloc, loc_layer, ws_bytes;
 };
 
@@ -142,6 +142,7 @@ Layout make_layout(const ham_config* c) {
   o = 0;
   const size_t R = y.rows_max;
   y.x = take((size_t)y.rows_dec * y.d * 4);
+  y.x2 = take((size_t)y.rows_dec * y.d * 4);  // second residual buffer (staged norms write the other one)
   y.xp = take((size_t)y.Tc * y.d * 4);
   // activation operands: 4 bytes per value (fp32, or a bf16 hi/lo pair)
   y.xn = take(R * std::max(y.d, y.HD) * 4);
@@ -150,6 +151,8 @@ Layout make_layout(const ham_config* c) {
   y.ao = take(R * y.HD * 4);
   y.act = take(R * y.F * 4);
   y.part = take((size_t)MAX_GEMM_SPLIT * 64 * y.Nmax * 4);
+  y.qpart = take((size_t)MAX_GEMM_SPLIT * 64 * y.QKV * 4);  // q/k/v partials (read while part is pending)
+  y.ssb = take((size_t)MAX_GEMM_SPLIT * 64 * 4);
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);
   y.apart = take(attn_part_bytes(y.rows_dec, y.H, y.Hk, y.hd));
@@ -308,22 +311,121 @@ struct StepAttn {
   int kv_cap;
 };
 
-// slot splits of the fused step: none while each wave holds at most four chunks
-// of key blocks; otherwise about two chunks per wave
-int attn_step_splits(int dtype, int Hk, int hd, int kv_cap) {
-  (void)Hk;
+// slot splits of the fused step.  A workgroup streams its share of the cache
+// at the rate of one compute unit, so small batches spread each (row, kv head)
+// over splits of a few key blocks until about 128 workgroups run; long
+// contexts split until every wave holds at most two chunks of key blocks.
+int attn_step_splits(int dtype, int R, int Hk, int hd, int kv_cap) {
   const int kb = dtype == HAM_BF16 ? 32 : 16;
   const int blocks = (kv_cap + kb - 1) / kb;
   const int chunk = 8 * (256 / hd);  // key blocks one workgroup holds in flight
-  if (blocks <= 4 * chunk) return 1;
-  return std::min(MAX_ATTN_SPLIT, (blocks + 2 * chunk - 1) / (2 * chunk));
+  const int for_length = (blocks + 2 * chunk - 1) / (2 * chunk);
+  const int for_width = std::min((128 + R * Hk - 1) / (R * Hk), (blocks + 1) / 2);
+  return std::max(1, std::min(MAX_ATTN_SPLIT, std::max(for_length, for_width)));
 }
 
 // one transformer layer (base layer j < L, micro layer j >= L) over R rows.
 // On entry `pend` may hold the previous layer's down-projection partials (folded
 // into x by the first norm, which also copies the updated rows to ctx_prev); on
 // exit it holds this layer's, if split.
-int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefill, void* Kc, void* VTc,
+// The fused decode path of one layer (rows of mode DECODE or MICROK): the first
+// RMSNorm folded into the q/k/v projection, the fused attention step, the
+// merge of the attention splits folded into the o-projection, the second
+// RMSNorm folded into gate/up.  Where a staged prologue does not fit, the
+// separate kernels run instead.  A folded norm writes the updated residual to
+// the other row buffer: `x` names the current one on entry and on exit.
+int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void* Kc, void* VTc, long long sb,
+                   long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
+                   float* ctx_prev, int ldctx, int kv_visible, const StepAttn& step, bool base) {
+  const Layout& y = m->y;
+  const int dt = dtype_of(m);
+  const auto gk = [&](int kind) { return base ? kind : HAM_PROF_MICRO; };
+  float* xa = m->WS<float>(y.x);
+  float* xb = m->WS<float>(y.x2);
+  const auto other = [&](float* p) { return p == xa ? xb : xa; };
+  const int split = MAX_GEMM_SPLIT;
+  const float eps = m->cfg.norm_eps;
+  int ns = 1;
+
+  // q/k/v projection, first norm folded in; its partials go to qpart
+  GemmArgs ga{};
+  ga.gate = gate; ga.gate_n = gate_n; ga.M = R;
+  ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
+  ga.part = m->WS<float>(y.qpart);
+  ga.xsrc = XS_NORM;
+  ga.xs.x = x; ga.xs.ldx = y.d; ga.xs.part = pend.part; ga.xs.nsplit = pend.nsplit; ga.xs.pM = pend.M;
+  ga.xs.g = m->W<float>(y.g1[j]); ga.xs.eps = eps; ga.xs.x_out = other(x); ga.xs.ctx = ctx_prev;
+  ga.xs.ldctx = ldctx; ga.xs.ss_out = m->WS<float>(y.ssb);
+  const int qkv_split = std::min(split, attn_step_max_qkv_split());
+  const bool q_staged = gemm_stage_fits(dt, EPI_F32, ga, qkv_split);
+  if (!q_staged) {
+    norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
+    ga.xsrc = XS_ACT; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+  }
+  if (gemm_p(m, EPI_F32, ga, qkv_split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
+  if (q_staged) {
+    x = other(x);
+    pend = Pending{};
+  }
+
+  // the o-projection takes the attention splits directly when its prologue fits
+  GemmArgs go{};
+  go.gate = gate; go.gate_n = gate_n; go.M = R; go.part = m->WS<float>(y.part);
+  go.W = m->W<char>(y.Wo[j]); go.N = y.d; go.K = y.HD; go.out = x; go.ldo = y.d;
+  go.xsrc = XS_ATTN;
+  go.xs.rec_o = m->WS<float>(y.apart);
+  go.xs.rec_ml = m->WS<float>(y.apart) + (size_t)R * y.Hk * attn_split * (y.H / y.Hk) * y.hd;
+  go.xs.ans = attn_split; go.xs.Hkv = y.Hk; go.xs.grp = y.H / y.Hk; go.xs.hd = y.hd;
+  const bool o_staged = attn_split > 1 && gemm_stage_fits(dt, EPI_RESID, go, split);
+
+  AttnStepArgs sa{};
+  sa.qkv = m->WS<float>(y.qkv); sa.part = ns > 1 ? m->WS<float>(y.qpart) : nullptr; sa.nsplit_qkv = ns;
+  sa.pM = R; sa.ldqkv = y.QKV;
+  sa.cos_p = step.cos_p; sa.sin_p = step.sin_p; sa.cs_stride = step.cs_stride;
+  sa.K = Kc; sa.VT = VTc; sa.sb = sb; sa.sh = sh; sa.S = S;
+  sa.H = y.H; sa.Hkv = y.Hk; sa.hd = y.hd; sa.R = R; sa.nsplit = attn_split; sa.kv_cap = step.kv_cap;
+  sa.o = m->WS<char>(y.ao); sa.ldo = y.HD; sa.part_out = m->WS<float>(y.apart); sa.rm = rm;
+  sa.combine = !o_staged;
+  sa.ss = (q_staged && ns > 1) ? m->WS<float>(y.ssb) : nullptr; sa.ss_n = ns; sa.d = y.d; sa.eps = eps;
+  m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
+  const int arc = launch_attn_step(dt, sa, m->s);
+  m->pend();
+  if (arc != 0) return fail(HAM_EINVAL, "attention step shape");
+
+  if (!o_staged) {
+    go.xsrc = XS_ACT; go.X = m->WS<char>(y.ao); go.ldx = y.HD;
+  }
+  if (gemm_p(m, EPI_RESID, go, split, gk(HAM_PROF_O), &ns)) return fail(HAM_EINVAL, "o-proj gemm shape");
+  if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
+
+  // gate/up, second norm folded in
+  GemmArgs gu{};
+  gu.gate = gate; gu.gate_n = gate_n; gu.M = R;
+  gu.W = m->W<char>(y.Wgu[j]); gu.N = 2 * y.F; gu.K = y.d; gu.out = m->WS<char>(y.act); gu.ldo = y.F;
+  gu.xsrc = XS_NORM;
+  gu.xs.x = x; gu.xs.ldx = y.d; gu.xs.part = pend.part; gu.xs.nsplit = pend.nsplit; gu.xs.pM = pend.M;
+  gu.xs.g = m->W<float>(y.g2[j]); gu.xs.eps = eps; gu.xs.x_out = other(x);
+  const bool u_staged = gemm_stage_fits(dt, EPI_SWIGLU, gu, 1);
+  if (!u_staged) {
+    norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n);
+    gu.xsrc = XS_ACT; gu.X = m->WS<char>(y.xn); gu.ldx = y.d;
+  }
+  if (gemm_p(m, EPI_SWIGLU, gu, 1, gk(HAM_PROF_GU), &ns)) return fail(HAM_EINVAL, "gate/up gemm shape");
+  if (u_staged) {
+    x = other(x);
+    pend = Pending{};
+  }
+
+  GemmArgs gd{};
+  gd.gate = gate; gd.gate_n = gate_n; gd.M = R; gd.part = m->WS<float>(y.part);
+  gd.W = m->W<char>(y.Wd[j]); gd.N = y.d; gd.K = y.F; gd.X = m->WS<char>(y.act); gd.ldx = y.F;
+  gd.out = x; gd.ldo = y.d;
+  if (gemm_p(m, EPI_RESID, gd, split, gk(HAM_PROF_DOWN), &ns)) return fail(HAM_EINVAL, "down gemm shape");
+  if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
+  return HAM_OK;
+}
+
+int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool prefill, void* Kc, void* VTc,
               long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
               float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step) {
   const Layout& y = m->y;
@@ -338,6 +440,9 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefi
     gate = nullptr;
     gate_n = 0;
   }
+  if (step)
+    return run_layer_step(m, j, R, rm, x, Kc, VTc, sb, sh, S, attn_split, gate, gate_n, pend, ctx_prev, ldctx,
+                          kv_visible, *step, base);
   const int split = prefill ? 1 : MAX_GEMM_SPLIT;
   int ns = 1;
   norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
@@ -346,23 +451,7 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float* x, bool prefi
   ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n;
   ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = R;
   ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
-  const int qkv_split = step ? std::min(split, attn_step_max_qkv_split()) : split;
-  if (gemm_p(m, EPI_F32, ga, qkv_split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
-
-  if (step) {
-    AttnStepArgs sa{};
-    sa.qkv = m->WS<float>(y.qkv); sa.part = ns > 1 ? m->WS<float>(y.part) : nullptr; sa.nsplit_qkv = ns;
-    sa.pM = R; sa.ldqkv = y.QKV;
-    sa.cos_p = step->cos_p; sa.sin_p = step->sin_p; sa.cs_stride = step->cs_stride;
-    sa.K = Kc; sa.VT = VTc; sa.sb = sb; sa.sh = sh; sa.S = S;
-    sa.H = y.H; sa.Hkv = y.Hk; sa.hd = y.hd; sa.R = R; sa.nsplit = attn_split; sa.kv_cap = step->kv_cap;
-    sa.o = m->WS<char>(y.ao); sa.ldo = y.HD; sa.part_out = m->WS<float>(y.apart); sa.rm = rm;
-    m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
-    const int arc = launch_attn_step(dt, sa, s);
-    m->pend();
-    if (arc != 0) return fail(HAM_EINVAL, "attention step shape");
-    return layer_tail(m, j, R, x, split, gate, gate_n, pend, gk);
-  }
+  if (gemm_p(m, EPI_F32, ga, split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
 
   RopeArgs ra{};
   ra.qkv = m->WS<float>(y.qkv); ra.ldqkv = y.QKV; ra.R = R; ra.q = m->WS<char>(y.q); ra.ldq = y.HD;
@@ -410,19 +499,19 @@ int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, con
 }
 
 // decision k = 0 from the base model, then the micro steps (all gated on device)
-int decode_tail(ham_model* m, Pending& pend, float* ctx_last, int* out_tokens, int* out_lens) {
+int decode_tail(ham_model* m, Pending& pend, float* ctx_last, float* xres, int* out_tokens, int* out_lens) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   const int B = m->batch;
-  float* x = m->WS<float>(y.x);
-  int rc = run_decision(m, 0, x, 1, 0, m->W<float>(y.gf), pend, ctx_last, out_tokens, out_lens);
+  int rc = run_decision(m, 0, xres, 1, 0, m->W<float>(y.gf), pend, ctx_last, out_tokens, out_lens);
   if (rc) return rc;
   const long long lsb = (long long)y.Hk * LOCAL_SLOTS * y.hd, lsh = (long long)LOCAL_SLOTS * y.hd;
   for (int k = 1; k < y.G; ++k) {
     MicroPrepArgs mp{};
     mp.st = m->sp; mp.B = B; mp.C = y.C; mp.k = k; mp.d = y.d; mp.ctx = m->WS<float>(y.ctx);
-    mp.E = m->W<char>(y.E); mp.x = x;
+    mp.E = m->W<char>(y.E); mp.x = m->WS<float>(y.x);
     launch_micro_prep(dt, mp, m->s);
+    float* x = m->WS<float>(y.x);  // micro-decoder rows start in the first residual buffer
     RowMap rm{};
     rm.mode = k == 1 ? ROWS_MICRO1 : ROWS_MICROK; rm.C = y.C; rm.k = k; rm.st = m->sp;
     const int R = k == 1 ? B * (y.C + 1) : B;
@@ -643,7 +732,7 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
     }
   }
   Pending none;
-  int rc = decode_tail(m, none, nullptr, d_out_tokens, d_out_lens);
+  int rc = decode_tail(m, none, nullptr, x, d_out_tokens, d_out_lens);
   if (rc) return rc;
   HIP_TRY(hipGetLastError());
   m->steps_done = 0;
@@ -704,7 +793,7 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   rm.mode = ROWS_DECODE; rm.st = m->sp;
   const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
   const int kv_max = m->prompt_len + m->steps_done + 1;  // every sequence holds at most this many slots now
-  const int nsplit = attn_step_splits(dt, y.Hk, y.hd, kv_max - 1);
+  const int nsplit = attn_step_splits(dt, B, y.Hk, y.hd, kv_max - 1);
   m->kv_visible = B * kv_max;
   const StepAttn bstep{m->WS<float>(y.rope_cs), m->WS<float>(y.rope_cs) + y.hd / 2, y.hd, kv_max - 1};
   float* ctx = m->WS<float>(y.ctx);
@@ -718,7 +807,7 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
     for (int c = 0; c < y.C; ++c)
       if (y.ctx_l[c] == l + 1) ctx_prev = ctx + (size_t)c * y.d;
   }
-  int rc = decode_tail(m, pend, ctx_prev, d_out_tokens, d_out_lens);
+  int rc = decode_tail(m, pend, ctx_prev, x, d_out_tokens, d_out_lens);
   if (rc) return rc;
   HIP_TRY(hipGetLastError());
   m->steps_done += 1;

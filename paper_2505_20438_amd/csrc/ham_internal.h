@@ -56,6 +56,31 @@ struct DecideArgs {
   int* best_idx;
 };
 
+// Where the skinny GEMM takes its X operand from.  XS_ACT: activation rows in
+// memory (storage-type planes).  The other two build X in LDS in a prologue of
+// the GEMM itself (rows M <= 8), so the kernel that would otherwise produce X
+// disappears from the launch sequence:
+//  XS_NORM: X = g * (x + pending split-K partials) * rinv, the RMSNorm of the
+//    updated residual.  With one k-split the workgroup sees the whole row and
+//    applies rinv itself; with several, X is left unscaled, each split reports
+//    the sum of squares of its k-range in ss_out, and the consumer of the
+//    output applies rinv.  Column tile 0 writes the updated rows to x_out
+//    (never x itself: other workgroups are still reading it) and to ctx.
+//  XS_ATTN: X = attention output combined from the split records of the
+//    decode attention (log-sum-exp weights per head, splits in order).
+enum XSource { XS_ACT = 0, XS_NORM = 1, XS_ATTN = 2 };
+struct XStage {
+  const float* x; int ldx;             // NORM: residual rows [M][ldx]
+  const float* part; int nsplit, pM;   // NORM: pending partials [nsplit][pM][ldx], or null
+  const float* g; float eps;           // NORM: gain [K]
+  float* x_out;                        // NORM: updated rows [M][ldx]
+  float* ctx; int ldctx;               // NORM: optional copy of the updated rows
+  float* ss_out;                       // NORM, k-split launches: [split][M] sums of squares
+  const float* rec_o;                  // ATTN: unnormalised outputs [M][Hkv][ans][grp][hd]
+  const float* rec_ml;                 // ATTN: (max, sum) [M][Hkv][ans][grp][2]
+  int ans, Hkv, grp, hd;               // ATTN: splits, heads, head dim
+};
+
 struct GemmArgs {
   const void* W; int N, K;         // W [N][K] row-major (storage type), N % 32 == 0
   const void* X; int ldx; int M;   // X [M][ldx] (storage type)
@@ -65,6 +90,7 @@ struct GemmArgs {
   const int* gate; int gate_n;     // launch does nothing unless a gate flag is set
   float* part; int* counters; int nsplit;  // split-K partials [nsplit][M][N] (written when nsplit > 1)
   DecideArgs dec;                  // ARGMAX only
+  int xsrc; XStage xs;             // X operand source (XS_ACT: X above)
 };
 
 // ---------------------------------------------------------------- attention
@@ -75,7 +101,7 @@ struct AttnArgs {
   int S;                           // slot capacity (row length of VT)
   int H, Hkv, hd, R, nsplit;
   void* o; int ldo;                // o [R][H*hd] (storage type)
-  float* part; int* counters;      // split partials [R][Hkv][nsplit][grp][hd+2]  (counters unused)
+  float* part; int* counters;      // split records: outputs [R][Hkv][nsplit][grp][hd], then (max, sum) [..][2]
   RowMap rm;
   const int* gate; int gate_n;
 };
@@ -89,7 +115,10 @@ struct AttnStepArgs {
   int H, Hkv, hd, R, nsplit;
   int kv_cap;                      // bound on the cached slots of every row (new slot excluded)
   void* o; int ldo;                // o [R][H*hd] (storage type)
-  float* part_out;                 // split partials [R][Hkv][nsplit][grp][hd+2]
+  float* part_out;                 // split records as in AttnArgs::part
+  bool combine;                    // merge split records into o here (else a staged GEMM does)
+  const float* ss; int ss_n, d;    // projection left unscaled: rinv = 1/sqrt(sum of ss[0..ss_n)[r] / d + eps)
+  float eps;
   RowMap rm;
 };
 
@@ -97,7 +126,11 @@ struct AttnStepArgs {
 typedef hipStream_t Stream;
 // tag 0: base-layer launch (distinct kernel name in profiles), 1: any other.
 // *nsplit receives the k-split used; above 1 the result is fp32 partials in a.part.
+// returns GEMM_NO_STAGE (nothing launched) when a staged X source does not fit
 int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, int tag, int* nsplit);
+constexpr int GEMM_NO_STAGE = -2;
+// whether launch_gemm would take the staged path for these arguments (nothing launched)
+bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split);
 int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s);
 int skinny_tiles(int N);  // column tiles (argmax partials per row) of a skinny launch over N columns
 int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s);

@@ -202,14 +202,18 @@ __device__ __forceinline__ void attn_publish(AttnLds<HD>& sh, int grp, float mru
   }
 }
 
+// Split records of the decode attention: unnormalised outputs
+// [R][Hkv][nsplit][grp][hd], then (max, sum) [R][Hkv][nsplit][grp][2].
+__device__ __forceinline__ size_t attn_rec(int r, int kvh, int split, int j, int Hkv, int nsplit, int grp) {
+  return (((size_t)r * Hkv + kvh) * nsplit + split) * grp + j;
+}
+
 // After a barrier: merge the waves in order (then the extra slot, if any); each
 // thread owns (q-head j, column d) pairs.  One split: normalised output; else
-// the split's (O, max, sum) record for k_attn_combine.
+// the split's record.
 template <typename T, int HD>
-__device__ __forceinline__ void attn_merge_store(const AttnLds<HD>& sh, bool extra, int grp, int r, int kvh,
+__device__ __forceinline__ void attn_merge_store(const AttnLds<HD>& sh, bool extra, int grp, int r, int R, int kvh,
                                                  int split, int nsplit, int Hkv, void* out, int ldo, float* part) {
-  const size_t rec = HD + 2;
-  float* pb = part + (((size_t)r * Hkv + kvh) * nsplit) * grp * rec;
   for (int t = threadIdx.x; t < grp * HD; t += 64 * ATTN_NW) {
     const int j = t / HD, d = t % HD;
     float M = extra ? sh.xs[j] : -INFINITY;
@@ -232,11 +236,12 @@ __device__ __forceinline__ void attn_merge_store(const AttnLds<HD>& sh, bool ext
     if (nsplit == 1) {
       Act<T>::put(out, r, ldo, (kvh * grp + j) * HD + d, L > 0.f ? O / L : 0.f);
     } else {
-      float* pj = pb + ((size_t)split * grp + j) * rec;
-      pj[d] = O;
+      const size_t q = attn_rec(r, kvh, split, j, Hkv, nsplit, grp);
+      part[q * HD + d] = O;
       if (d == 0) {
-        pj[HD] = M;
-        pj[HD + 1] = L;
+        float* ml = part + (size_t)R * Hkv * nsplit * grp * HD + 2 * q;
+        ml[0] = M;
+        ml[1] = L;
       }
     }
   }
@@ -279,7 +284,7 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_decode(AttnArgs a) {
   attn_blocks<T, HD>(Kb, Vb, a.S, s0, b0, b1, s1, s1, qf, ql, scale, mrun, lrun, o);
   attn_publish<T, HD>(sh, grp, mrun, lrun, o);
   __syncthreads();
-  attn_merge_store<T, HD>(sh, false, grp, r, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part);
+  attn_merge_store<T, HD>(sh, false, grp, r, a.R, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part);
 }
 
 // ---------------------------------------------------------------- fused decode step
@@ -342,6 +347,17 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) sraw[c + e] = acc[e];
   }
+  // RMSNorm scale of this row when the projection's input was left unscaled
+  float rinv = 1.f;
+  if (a.ss) {
+    float sv[MAXS];
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) sv[s] = s < a.ss_n ? a.ss[(size_t)s * a.pM + r] : 0.f;
+    float ss = 0.f;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) ss += sv[s];
+    rinv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+  }
   // RoPE factors of this row: elements i = f*KB + g*EPL + e, f < NF/2
   const float* cp = a.cos_p + (size_t)r * a.cs_stride;
   const float* sp = a.sin_p + (size_t)r * a.cs_stride;
@@ -366,8 +382,8 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
   for (int f = 0; f < NF; ++f)
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      qv[f][e] = sraw[qh * HD + f * KB + g * EPL + e];
-      kv[f][e] = sraw[grp * HD + f * KB + g * EPL + e];
+      qv[f][e] = sraw[qh * HD + f * KB + g * EPL + e] * rinv;
+      kv[f][e] = sraw[grp * HD + f * KB + g * EPL + e] * rinv;
     }
 #pragma unroll
   for (int f = 0; f < NF / 2; ++f)
@@ -429,7 +445,7 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
       }
     }
     for (int d = threadIdx.x; d < HD; d += 64 * ATTN_NW) {
-      const T v = from_f<T>(sraw[(grp + 1) * HD + d]);
+      const T v = from_f<T>(sraw[(grp + 1) * HD + d] * rinv);
       sh.xv[d] = to_f<T>(v);
       ((T*)a.VT)[(size_t)r * a.sb + kvh * a.sh + (size_t)d * a.S + ri.slot] = v;
     }
@@ -446,7 +462,7 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
   attn_blocks<T, HD>(Kb, Vb, a.S, 0, b0 + NB, b1, limit, limit, qf, ql, scale, mrun, lrun, o);
   attn_publish<T, HD>(sh, grp, mrun, lrun, o);
   __syncthreads();
-  attn_merge_store<T, HD>(sh, extra, grp, r, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part_out);
+  attn_merge_store<T, HD>(sh, extra, grp, r, a.R, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part_out);
 }
 
 // Log-sum-exp combine of the splits of one (row, head), in split order.
@@ -455,19 +471,18 @@ __global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int grp = a.H / a.Hkv, kvh = h / grp, j = h % grp, HD = a.hd;
-  const size_t rec = HD + 2;
-  const float* pb = a.part + (((size_t)r * a.Hkv + kvh) * a.nsplit) * grp * rec;
+  const float* ml = a.part + (size_t)a.R * a.Hkv * a.nsplit * grp * HD;
   float M = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, pb[((size_t)s * grp + j) * rec + HD]);
+  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, ml[2 * attn_rec(r, kvh, s, j, a.Hkv, a.nsplit, grp)]);
   for (int d = lane; d < HD; d += 64) {
     float L = 0.f, O = 0.f;
     if (M != -INFINITY) {
       for (int s = 0; s < a.nsplit; ++s) {
-        const float* ps = pb + ((size_t)s * grp + j) * rec;
-        const float ms = ps[HD];
+        const size_t q = attn_rec(r, kvh, s, j, a.Hkv, a.nsplit, grp);
+        const float ms = ml[2 * q];
         const float wgt = ms == -INFINITY ? 0.f : __expf(ms - M);
-        L += wgt * ps[HD + 1];
-        O += wgt * ps[d];
+        L += wgt * ml[2 * q + 1];
+        O += wgt * a.part[q * HD + d];
       }
     }
     Act<T>::put(a.o, r, a.ldo, h * HD + d, L > 0.f ? O / L : 0.f);
@@ -541,7 +556,7 @@ static int step_t(const AttnStepArgs& a, Stream s) {
   if (a.hd == 64) hipLaunchKernelGGL((k_attn_step<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else if (a.hd == 128) hipLaunchKernelGGL((k_attn_step<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else return -1;
-  if (a.nsplit > 1) {
+  if (a.nsplit > 1 && a.combine) {
     AttnArgs c{};
     c.H = a.H; c.Hkv = a.Hkv; c.hd = a.hd; c.R = a.R; c.nsplit = a.nsplit; c.o = a.o; c.ldo = a.ldo;
     c.part = a.part_out;

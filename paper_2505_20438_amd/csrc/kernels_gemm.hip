@@ -95,6 +95,10 @@ __device__ __forceinline__ void skinny_mma(f4 (*acc)[TN], const SkinnyBatch<T, M
       for (int j = 0; j < TN; ++j) mma_act<T>(acc[i][j], b.xh[u][i], b.xl[u][i], b.w[u][j]);
 }
 
+template <typename T, int MT, int TN, int EPI, int NW>
+__device__ __forceinline__ void skinny_finish(const GemmArgs& a, f4 (*acc)[TN], float* red, int ntile, int split,
+                                              int nsplit, int n0);
+
 // TAG only separates the names of base-layer launches (always active) from the
 // others in profiler output; the code is the same.
 template <typename T, int MT, int TN, int EPI, int TAG>
@@ -103,7 +107,7 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB;
   constexpr int NACC = MT * TN * 4;
   constexpr int U = SkinnyBatch<T, MT, TN>::U;
-  __shared__ float red[3][NACC][64];
+  __shared__ float red[3][NACC][64];  // k-slices of waves 1..3
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int ntile = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
@@ -160,14 +164,25 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
     }
   }
 
-  // reduce the four waves' k-slices (fixed order: wave 0 + 1 + 2 + 3)
+  skinny_finish<T, MT, TN, EPI, 4>(a, acc, &red[0][0][0], ntile, split, nsplit, n0);
+}
+
+// Reduction of the NW waves' k-slices of one workgroup (fixed order: wave 0,
+// 1, ...; red holds [NW-1][NACC][64] floats) and the epilogue: split partials,
+// the LM head's per-tile argmax, or the fused epilogue.
+template <typename T, int MT, int TN, int EPI, int NW>
+__device__ __forceinline__ void skinny_finish(const GemmArgs& a, f4 (*acc)[TN], float* red, int ntile, int split,
+                                              int nsplit, int n0) {
+  constexpr int NACC = MT * TN * 4;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
   if (w > 0) {
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[w - 1][(i * TN + j) * 4 + r][lane] = acc[i][j][r];
+        for (int r = 0; r < 4; ++r) red[((w - 1) * NACC + (i * TN + j) * 4 + r) * 64 + lane] = acc[i][j][r];
   }
   __syncthreads();
   if (w != 0) return;
@@ -178,9 +193,11 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int q = (i * TN + j) * 4 + r;
-        acc[i][j][r] = ((acc[i][j][r] + red[0][q][lane]) + red[1][q][lane]) + red[2][q][lane];
+        float v = acc[i][j][r];
+#pragma unroll
+        for (int p = 0; p < NW - 1; ++p) v += red[(p * NACC + q) * 64 + lane];
+        acc[i][j][r] = v;
       }
-
   if (nsplit > 1) {  // partial of this k-chunk; the consumer sums the chunks in order
 #pragma unroll
     for (int i = 0; i < MT; ++i)
@@ -240,6 +257,271 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
           epi_tile<T, EPI>(a, m, m < a.M, n0 + 16 * j, r16, acc[i][j][r]);
         }
   }
+}
+
+
+// ------------------------------------------------------------------------ staged
+// Skinny GEMM whose X operand is built in LDS by a prologue (XStage): eight
+// waves split the k-range of a 16*TN-column tile; the first batch of weight
+// loads is issued before the prologue so both are in flight together.
+// Rows M <= 8 and M * (k-range) <= STG_VALS values.
+constexpr int STG_NW = 8;
+constexpr int STG_THREADS = 64 * STG_NW;
+constexpr int STG_CH = 2;                         // 4-value chunks of X per thread
+constexpr int STG_VALS = STG_CH * STG_THREADS * 4;  // X values one workgroup stages
+constexpr int STG_SMAX = 8;                       // pending partials summed by the NORM prologue
+constexpr int STG_AMAX = 8;                       // attention splits one thread combines
+constexpr int STG_MMAX = 8;
+
+// 4 consecutive values of X row m at local column kl -> the LDS operand layout
+// (bf16: hi plane then lo plane per row, 4 bytes per value in total; fp32: as is)
+template <typename T>
+__device__ __forceinline__ void stage_put4(char* stg, int Kr, int m, int kl, f4 v);
+template <>
+__device__ __forceinline__ void stage_put4<bf16>(char* stg, int Kr, int m, int kl, f4 v) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bf16 hb = f2bf(v[e]);
+    h[e] = hb;
+    l[e] = f2bf(v[e] - bf2f(hb));
+  }
+  char* row = stg + (size_t)m * 4 * Kr;
+  *reinterpret_cast<uint2*>(row + (size_t)kl * 2) = uint2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+  *reinterpret_cast<uint2*>(row + (size_t)2 * Kr + (size_t)kl * 2) = uint2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
+}
+template <>
+__device__ __forceinline__ void stage_put4<float>(char* stg, int Kr, int m, int kl, f4 v) {
+  *reinterpret_cast<f4*>(stg + (size_t)m * 4 * Kr + (size_t)kl * 4) = v;
+}
+
+// XS_NORM prologue.  Chunk i (of M * Kr/4) is row i / (Kr/4), columns k0 + 4*(i % (Kr/4)).
+// aux: [nch] chunk sums of squares, then [M] row sums.
+template <typename T>
+__device__ __forceinline__ void stage_norm(const GemmArgs& a, char* stg, float* aux, int k0, int Kr, int split,
+                                           bool tile0) {
+  const XStage& s = a.xs;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int M = a.M, cpr = Kr / 4, nch = M * cpr;
+  const int ns = s.part ? s.nsplit : 0;
+  const bool whole = gridDim.y == 1;  // the workgroup sees whole rows: apply rinv here
+  f4 v[STG_CH], gv[STG_CH];
+  f4 pv[STG_CH][STG_SMAX];
+#pragma unroll
+  for (int j = 0; j < STG_CH; ++j) {
+    const int i = tid + j * STG_THREADS;
+    if (i < nch) {
+      const int m = i / cpr, k = k0 + (i % cpr) * 4;
+      v[j] = *reinterpret_cast<const f4*>(s.x + (size_t)m * s.ldx + k);
+      gv[j] = *reinterpret_cast<const f4*>(s.g + k);
+#pragma unroll
+      for (int q = 0; q < STG_SMAX; ++q)
+        if (q < ns) pv[j][q] = *reinterpret_cast<const f4*>(s.part + ((size_t)q * s.pM + m) * s.ldx + k);
+    }
+  }
+  float* sq = aux;
+  float* ssr = aux + nch;
+#pragma unroll
+  for (int j = 0; j < STG_CH; ++j) {
+    const int i = tid + j * STG_THREADS;
+    if (i < nch) {
+#pragma unroll
+      for (int q = 0; q < STG_SMAX; ++q)
+        if (q < ns) v[j] += pv[j][q];
+      const f4 x = v[j];
+      sq[i] = (x[0] * x[0] + x[1] * x[1]) + (x[2] * x[2] + x[3] * x[3]);
+      if (tile0) {
+        const int m = i / cpr, k = k0 + (i % cpr) * 4;
+        *reinterpret_cast<f4*>(s.x_out + (size_t)m * s.ldx + k) = x;
+        if (s.ctx) *reinterpret_cast<f4*>(s.ctx + (size_t)m * s.ldctx + k) = x;
+      }
+    }
+  }
+  __syncthreads();
+  if (w < M) {  // wave m: the sum of squares of row m over this k-range, fixed order
+    float t = 0.f;
+    for (int c = lane; c < cpr; c += 64) t += sq[w * cpr + c];
+    t = wave_sum(t);
+    if (lane == 0) ssr[w] = t;
+  }
+  __syncthreads();
+  if (!whole && tile0 && tid < M) s.ss_out[(size_t)split * M + tid] = ssr[tid];
+#pragma unroll
+  for (int j = 0; j < STG_CH; ++j) {
+    const int i = tid + j * STG_THREADS;
+    if (i < nch) {
+      const int m = i / cpr, kl = (i % cpr) * 4;
+      const float sc = whole ? 1.0f / sqrtf(ssr[m] / (float)a.K + s.eps) : 1.0f;
+      stage_put4<T>(stg, Kr, m, kl, v[j] * sc * gv[j]);
+    }
+  }
+}
+
+// XS_ATTN prologue.  Heads h0.. of the k-range; one wave per (row, head)
+// forms the softmax weights exp(m_s - M) / L of the splits (lane s holds split
+// s), then thread (chunk c, group sg) sums the weighted outputs of splits sg,
+// sg + SG, ... and the groups are added in order.  aux: [M][nh][ans] weights,
+// then [SG][nch] 4-value partial sums.
+template <typename T>
+__device__ __forceinline__ void stage_attn(const GemmArgs& a, char* stg, float* aux, int k0, int Kr) {
+  const XStage& s = a.xs;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int M = a.M, hd = s.hd, ans = s.ans, grp = s.grp, Hkv = s.Hkv;
+  const int h0 = k0 / hd, nh = (k0 + Kr - 1) / hd + 1 - h0;
+  const int cpr = Kr / 4, nch = M * cpr;
+  const int SG = max(1, min(STG_THREADS / nch, ans));
+  float* wts = aux;
+  f4* ps = reinterpret_cast<f4*>(aux + ((M * nh * ans + 3) & ~3));
+  // the outputs this thread combines, in flight while the weights are formed
+  const int c = tid % nch, sg = tid / nch;
+  const bool act = tid < nch * SG;
+  const int m = c / cpr, k = k0 + (c % cpr) * 4, h = k / hd, d = k % hd;
+  f4 o[STG_AMAX];
+  if (act) {
+    const float* ob = s.rec_o + ((((size_t)m * Hkv + h / grp) * ans) * grp + h % grp) * hd + d;
+#pragma unroll
+    for (int q = 0; q < STG_AMAX; ++q) {
+      const int sp = sg + q * SG;
+      if (sp < ans) o[q] = *reinterpret_cast<const f4*>(ob + (size_t)sp * grp * hd);
+    }
+  }
+  for (int gi = w; gi < M * nh; gi += STG_NW) {
+    const int gm = gi / nh, gh = h0 + gi % nh;
+    float ms = -INFINITY, ls = 0.f;
+    if (lane < ans) {
+      const size_t q = (((size_t)gm * Hkv + gh / grp) * ans + lane) * grp + gh % grp;
+      ms = s.rec_ml[2 * q];
+      ls = s.rec_ml[2 * q + 1];
+    }
+    const float Mx = wave_max(ms);
+    const float e = (ms == -INFINITY) ? 0.f : __expf(ms - Mx);
+    const float L = wave_sum(e * ls);
+    if (lane < ans) wts[gi * ans + lane] = L > 0.f ? e / L : 0.f;
+  }
+  __syncthreads();
+  if (act) {
+    const float* wt = wts + (m * nh + (h - h0)) * ans;
+    f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < STG_AMAX; ++q) {
+      const int sp = sg + q * SG;
+      if (sp < ans) acc += wt[sp] * o[q];
+    }
+    ps[tid] = acc;
+  }
+  __syncthreads();
+  for (int i = tid; i < nch; i += STG_THREADS) {
+    f4 x = ps[i];
+    for (int q = 1; q < SG; ++q) x += ps[q * nch + i];
+    stage_put4<T>(stg, Kr, i / cpr, (i % cpr) * 4, x);
+  }
+}
+
+// LDS bytes of a staged launch: wave reduction, X rows, prologue scratch
+__host__ __device__ inline size_t stage_lds_bytes(int tn, int M, int Kr, int xsrc, int ans, int hd) {
+  const size_t red = (size_t)(STG_NW - 1) * tn * 4 * 64 * 4;
+  const size_t stg = (size_t)M * Kr * 4;
+  const int nch = M * Kr / 4;
+  size_t aux;
+  if (xsrc == XS_NORM) {
+    aux = (size_t)(nch + STG_MMAX) * 4;
+  } else {
+    const int nh = Kr / hd + 2, nml = M * nh * ans;
+    aux = (size_t)((nml + 3) & ~3) * 4 + (size_t)STG_THREADS * 16;
+  }
+  return red + stg + aux;
+}
+
+template <typename T, int TN, int EPI, int TAG, int XS>
+__global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, U = 4;
+  extern __shared__ float dsm[];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int ntile = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
+  const int n0 = ntile * 16 * TN;
+  const int nfr = a.K / KB;
+  const int c0 = (int)((long)split * nfr / nsplit), c1 = (int)((long)(split + 1) * nfr / nsplit);
+  const int Kr = (c1 - c0) * KB;
+  const int f0 = c0 + w * (c1 - c0) / STG_NW, f1 = c0 + (w + 1) * (c1 - c0) / STG_NW;
+  float* red = dsm;
+  char* stg = reinterpret_cast<char*>(dsm + (STG_NW - 1) * TN * 4 * 64);
+  float* aux = reinterpret_cast<float*>(stg + (size_t)a.M * 4 * Kr);
+  const T* W = (const T*)a.W;
+  const T* wrow[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) wrow[j] = W + (size_t)(n0 / 16 + j) * nfr * 64 * EPL + (size_t)lane * EPL;
+  // the wave's first PF weight fragments are in flight before the prologue starts
+  // (8 blocks in all: more would cost the occupancy of two workgroups per CU)
+  constexpr int PF = 8 / TN;
+  const int npf = min(PF, f1 - f0);
+  u4 wp[PF][TN];
+#pragma unroll
+  for (int u = 0; u < PF; ++u)
+    if (u < npf) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wp[u][j] = ld16_stream(wrow[j] + (size_t)(f0 + u) * 64 * EPL);
+    }
+  if constexpr (XS == XS_NORM) stage_norm<T>(a, stg, aux, c0 * KB, Kr, split, ntile == 0);
+  else stage_attn<T>(a, stg, aux, c0 * KB, Kr);
+  __syncthreads();
+  // the rest in batches of U, the first batch issued before the prefetched ones are used
+  const int fr0 = f0 + npf;
+  const int nb = (f1 - fr0) / U;
+  u4 wc[U][TN], wn[U][TN];
+  auto wload = [&](u4 (*dst)[TN], int f) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) dst[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * 64 * EPL);
+  };
+  if (nb > 0) wload(wc, fr0);
+
+  const bool xrow = r16 < a.M;
+  const char* xb = stg + (size_t)(xrow ? r16 : 0) * 4 * Kr + (size_t)g * EPL * sizeof(T);
+  auto xfrag = [&](int f, u4& h, u4& l) {
+    const char* p = xb + (size_t)(f - c0) * KB * sizeof(T);
+    h = xrow ? *reinterpret_cast<const u4*>(p) : zero16();
+    l = (Act<T>::SPLIT && xrow) ? *reinterpret_cast<const u4*>(p + 2 * Kr) : zero16();
+  };
+  f4 acc[1][TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) acc[0][j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < PF; ++u)
+    if (u < npf) {
+      u4 h, l;
+      xfrag(f0 + u, h, l);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, wp[u][j]);
+    }
+  for (int it = 0; it < nb; ++it) {
+    const bool more = it + 1 < nb;
+    if (more) wload(wn, fr0 + (it + 1) * U);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      u4 h, l;
+      xfrag(fr0 + it * U + u, h, l);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, wc[u][j]);
+    }
+    if (more) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) wc[u][j] = wn[u][j];
+    }
+  }
+  for (int f = fr0 + nb * U; f < f1; ++f) {
+    u4 bw[TN], h, l;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * 64 * EPL);
+    xfrag(f, h, l);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, bw[j]);
+  }
+  skinny_finish<T, 1, TN, EPI, STG_NW>(a, acc, red, ntile, split, nsplit, n0);
 }
 
 // Final argmax of one row over all column tiles (fixed total order: larger value,
@@ -414,12 +696,71 @@ static void run_skinny_mt(const GemmArgs& a, int nsplit, int tag, Stream s) {
   else run_skinny<T, 4, TN, EPI>(a, nsplit, tag, s);
 }
 
+template <typename T, int TN, int EPI, int XS>
+static void run_staged(const GemmArgs& a, int nsplit, int tag, size_t lds, Stream s) {
+  dim3 grid(a.N / (16 * TN), nsplit);
+  if (!tag) hipLaunchKernelGGL((k_gemm_staged<T, TN, EPI, 0, XS>), grid, dim3(STG_THREADS), lds, s, a);
+  else hipLaunchKernelGGL((k_gemm_staged<T, TN, EPI, 1, XS>), grid, dim3(STG_THREADS), lds, s, a);
+}
+
+// Staged launch (X built in LDS): k-split and the checks that the prologue fits.
+// Returns GEMM_NO_STAGE if it does not; launches unless dry.
 template <typename T, int EPI>
-static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsplit_out) {
+static int gemm_staged(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsplit_out, bool dry) {
+  constexpr int KB = Frag<T>::KB;
+  GemmArgs a = a0;
+  constexpr bool norm_ok = EPI == EPI_F32 || EPI == EPI_SWIGLU;
+  constexpr bool attn_ok = EPI == EPI_RESID;
+  if ((a.xsrc == XS_NORM && !norm_ok) || (a.xsrc == XS_ATTN && !attn_ok)) return GEMM_NO_STAGE;
+  if (a.M > STG_MMAX) return GEMM_NO_STAGE;
+  const int nfr = a.K / KB;
+  const int ntiles = skinny_tiles(a.N);
+  const int TN = a.N / (16 * ntiles);
+  int nsplit = 1;
+  if (EPI != EPI_SWIGLU && max_split > 1) {
+    // at most about 512 workgroups (two per CU fit at once), two fragments per wave
+    nsplit = std::max(1, 512 / ntiles);
+    nsplit = std::max(1, std::min(nsplit, std::min(max_split, nfr / (2 * STG_NW))));
+  }
+  const int Kr = (nfr + nsplit - 1) / nsplit * KB;  // longest k-range
+  if (a.M * Kr > STG_VALS) return GEMM_NO_STAGE;
+  if (a.xsrc == XS_NORM) {
+    if (a.xs.part && (a.xs.nsplit < 1 || a.xs.nsplit > STG_SMAX)) return GEMM_NO_STAGE;
+    if (nsplit > 1 && !a.xs.ss_out) return GEMM_NO_STAGE;
+  } else {
+    const int nch = a.M * Kr / 4, ans = a.xs.ans;
+    if (nch > STG_THREADS || ans > 64) return GEMM_NO_STAGE;
+    const int SG = std::max(1, std::min(STG_THREADS / nch, ans));
+    if ((ans + SG - 1) / SG > STG_AMAX) return GEMM_NO_STAGE;
+  }
+  const size_t lds = stage_lds_bytes(TN, a.M, Kr, a.xsrc, a.xs.ans, a.xs.hd);
+  if (lds > 64 * 1024) return GEMM_NO_STAGE;
+  *nsplit_out = nsplit;
+  if (dry) return 0;
+  a.nsplit = nsplit;
+  if constexpr (norm_ok) {
+    if (TN == 2) run_staged<T, 2, EPI, XS_NORM>(a, nsplit, tag, lds, s);
+    else run_staged<T, 1, EPI, XS_NORM>(a, nsplit, tag, lds, s);
+  } else if constexpr (attn_ok) {
+    if (TN == 2) run_staged<T, 2, EPI, XS_ATTN>(a, nsplit, tag, lds, s);
+    else run_staged<T, 1, EPI, XS_ATTN>(a, nsplit, tag, lds, s);
+  }
+  return 0;
+}
+
+template <typename T, int EPI>
+static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsplit_out, bool dry = false) {
   GemmArgs a = a0;
   constexpr int KB = Frag<T>::KB;
   if (a.N % 32 != 0 || a.K % KB != 0 || a.M <= 0) return -1;
   *nsplit_out = 1;
+  if (a.xsrc != XS_ACT) {
+    if constexpr (EPI == EPI_F32 || EPI == EPI_SWIGLU || EPI == EPI_RESID)
+      return gemm_staged<T, EPI>(a, max_split, tag, s, nsplit_out, dry);
+    else
+      return GEMM_NO_STAGE;
+  }
+  if (dry) return GEMM_NO_STAGE;
   if (a.M > 64) {
     if constexpr (EPI == EPI_ARGMAX) {
       return -1;
@@ -447,24 +788,31 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
 }
 
 template <typename T>
-static int gemm_dispatch(int epi, const GemmArgs& a, int max_split, int tag, Stream s, int* ns) {
+static int gemm_dispatch(int epi, const GemmArgs& a, int max_split, int tag, Stream s, int* ns, bool dry) {
   switch (epi) {
-    case EPI_F32: return gemm_t<T, EPI_F32>(a, max_split, tag, s, ns);
-    case EPI_OP: return gemm_t<T, EPI_OP>(a, max_split, tag, s, ns);
-    case EPI_RESID: return gemm_t<T, EPI_RESID>(a, max_split, tag, s, ns);
-    case EPI_SWIGLU: return gemm_t<T, EPI_SWIGLU>(a, max_split, tag, s, ns);
-    case EPI_ARGMAX: return gemm_t<T, EPI_ARGMAX>(a, max_split, tag, s, ns);
-    case EPI_XMASK: return gemm_t<T, EPI_XMASK>(a, max_split, tag, s, ns);
+    case EPI_F32: return gemm_t<T, EPI_F32>(a, max_split, tag, s, ns, dry);
+    case EPI_OP: return gemm_t<T, EPI_OP>(a, max_split, tag, s, ns, dry);
+    case EPI_RESID: return gemm_t<T, EPI_RESID>(a, max_split, tag, s, ns, dry);
+    case EPI_SWIGLU: return gemm_t<T, EPI_SWIGLU>(a, max_split, tag, s, ns, dry);
+    case EPI_ARGMAX: return gemm_t<T, EPI_ARGMAX>(a, max_split, tag, s, ns, dry);
+    case EPI_XMASK: return gemm_t<T, EPI_XMASK>(a, max_split, tag, s, ns, dry);
   }
   return -1;
 }
 
 int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, int tag, int* nsplit) {
   int ns = 1;
-  const int rc = dtype == 1 ? gemm_dispatch<bf16>(epi, a, max_split, tag, s, &ns)
-                            : gemm_dispatch<float>(epi, a, max_split, tag, s, &ns);
+  const int rc = dtype == 1 ? gemm_dispatch<bf16>(epi, a, max_split, tag, s, &ns, false)
+                            : gemm_dispatch<float>(epi, a, max_split, tag, s, &ns, false);
   if (nsplit) *nsplit = ns;
   return rc;
+}
+
+bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split) {
+  int ns = 1;
+  const int rc = dtype == 1 ? gemm_dispatch<bf16>(epi, a, max_split, 1, nullptr, &ns, true)
+                            : gemm_dispatch<float>(epi, a, max_split, 1, nullptr, &ns, true);
+  return rc == 0;
 }
 
 int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s) {

@@ -145,12 +145,13 @@ __device__ __forceinline__ float block_sum256(float v, float* sh4) {
   return (sh4[0] + sh4[1]) + (sh4[2] + sh4[3]);
 }
 
-// any nonzero among n flags (n small); used to skip work no sequence needs
+// any nonzero among n <= 64 flags (one load per lane, then a wave vote; every
+// wave of a workgroup reaches the same answer); used to skip work no sequence needs
 __device__ __forceinline__ bool any_flag(const int* flags, int n) {
   if (flags == nullptr) return true;
-  for (int i = 0; i < n; ++i)
-    if (flags[i]) return true;
-  return false;
+  const int lane = threadIdx.x & 63;
+  const int v = lane < n ? flags[lane] : 0;
+  return __ballot(v != 0) != 0ull;
 }
 
 }  // namespace ham

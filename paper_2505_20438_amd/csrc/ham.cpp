@@ -19,6 +19,13 @@
 
 using namespace ham;
 
+namespace ham {
+LaunchTiming& launch_timing() {
+  static thread_local LaunchTiming t;
+  return t;
+}
+}  // namespace ham
+
 namespace {
 
 thread_local std::string g_err;
@@ -201,19 +208,20 @@ struct ham_model {
   int prof_kind = -1;
   double prof_bytes = 0;
   hipEvent_t prof_a = nullptr;
+  // the next kernel launched is timed by events attached to its dispatch
   void pbegin(int kind, double bytes) {
-    if (!prof_on) return;
+    if (!prof_on || kind < 0) return;
     prof_kind = kind;
     prof_bytes = bytes;
     prof_a = ev();
-    if (prof_a) hipEventRecord(prof_a, s);
+    hipEvent_t b = ev();
+    if (prof_a && b) launch_timing() = LaunchTiming{prof_a, b};
   }
   void pend() {
     if (!prof_on || !prof_a) return;
-    hipEvent_t b = ev();
-    if (!b) return;
-    hipEventRecord(b, s);
-    recs.push_back(Rec{prof_kind, prof_a, b, prof_bytes});
+    LaunchTiming& t = launch_timing();
+    if (!t.start) recs.push_back(Rec{prof_kind, prof_a, pool[pool_used - 1], prof_bytes});
+    t = LaunchTiming{};  // nothing was launched: disarm
     prof_a = nullptr;
   }
   ~ham_model() {
@@ -386,6 +394,7 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   sa.H = y.H; sa.Hkv = y.Hk; sa.hd = y.hd; sa.R = R; sa.nsplit = attn_split; sa.kv_cap = step.kv_cap;
   sa.o = m->WS<char>(y.ao); sa.ldo = y.HD; sa.part_out = m->WS<float>(y.apart); sa.rm = rm;
   sa.combine = !o_staged;
+  sa.gate = gate; sa.gate_n = gate_n;
   sa.ss = (q_staged && ns > 1) ? m->WS<float>(y.ssb) : nullptr; sa.ss_n = ns; sa.d = y.d; sa.eps = eps;
   m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
   const int arc = launch_attn_step(dt, sa, m->s);

@@ -1,10 +1,30 @@
 // Internal interfaces between the host orchestration (ham.cpp) and the kernels.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace ham {
+
+// Optional timing of the next kernel launch.  When armed, the launch helper
+// attaches the two events to the kernel's dispatch itself (its start and end,
+// without the queueing before it), then disarms.  One per host thread.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchTiming& launch_timing();
+
+template <typename... KArgs, typename... Args>
+inline void launch_k(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t s, Args... args) {
+  LaunchTiming& t = launch_timing();
+  if (t.start) {
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, t.start, t.stop, 0u, args...);
+    t = LaunchTiming{};
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+  }
+}
 
 // ---------------------------------------------------------------- per-sequence state
 // Structure-of-arrays in the state buffer, each int32 [max_batch] (grp_tok, teacher:
@@ -120,6 +140,7 @@ struct AttnStepArgs {
   const float* ss; int ss_n, d;    // projection left unscaled: rinv = 1/sqrt(sum of ss[0..ss_n)[r] / d + eps)
   float eps;
   RowMap rm;
+  const int* gate; int gate_n;     // launch does nothing unless a gate flag is set (micro steps)
 };
 
 // ---------------------------------------------------------------- launchers

@@ -323,6 +323,7 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
 #pragma unroll
   for (int i = 0; i < NB; ++i)
     if (b0 + i < b1) kv_load<T, HD>(blk[i], Kb, Vb, a.S, (b0 + i) * KB);
+  if (!any_flag(a.gate, a.gate_n)) return;
   const RowInfo ri = row_info(a.rm, r);
   // the projection values of this kv head: one 4-float chunk per thread, all splits
   const int nch = (grp + 2) * HD / 4;
@@ -535,17 +536,17 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
 template <typename T>
 static int decode_t(const AttnArgs& a, Stream s) {
   dim3 grid(a.nsplit, a.Hkv, a.R);
-  if (a.hd == 64) hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
-  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  if (a.hd == 64) launch_k((k_attn_decode<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  else if (a.hd == 128) launch_k((k_attn_decode<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else return -1;
-  if (a.nsplit > 1) hipLaunchKernelGGL((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, a);
+  if (a.nsplit > 1) launch_k((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, a);
   return 0;
 }
 template <typename T>
 static int prefill_t(const AttnArgs& a, Stream s) {
   dim3 grid((a.R + 63) / 64, a.H);
-  if (a.hd == 64) hipLaunchKernelGGL((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, a);
-  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, a);
+  if (a.hd == 64) launch_k((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, a);
+  else if (a.hd == 128) launch_k((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, a);
   else return -1;
   return 0;
 }
@@ -553,14 +554,14 @@ static int prefill_t(const AttnArgs& a, Stream s) {
 template <typename T>
 static int step_t(const AttnStepArgs& a, Stream s) {
   dim3 grid(a.nsplit, a.Hkv, a.R);
-  if (a.hd == 64) hipLaunchKernelGGL((k_attn_step<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
-  else if (a.hd == 128) hipLaunchKernelGGL((k_attn_step<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  if (a.hd == 64) launch_k((k_attn_step<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
+  else if (a.hd == 128) launch_k((k_attn_step<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else return -1;
   if (a.nsplit > 1 && a.combine) {
     AttnArgs c{};
     c.H = a.H; c.Hkv = a.Hkv; c.hd = a.hd; c.R = a.R; c.nsplit = a.nsplit; c.o = a.o; c.ldo = a.ldo;
     c.part = a.part_out;
-    hipLaunchKernelGGL((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, c);
+    launch_k((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, c);
   }
   return 0;
 }

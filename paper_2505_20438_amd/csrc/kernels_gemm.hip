@@ -525,20 +525,34 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
 }
 
 // Final argmax of one row over all column tiles (fixed total order: larger value,
-// then lower index), then the decision and stop test of that sequence.
-__global__ __launch_bounds__(256) void k_decide(DecideArgs d, int ntiles, int M) {
+// then lower index), then the decision and stop test of that sequence.  Each
+// thread issues all of its tile loads before comparing any of them.
+constexpr int DECIDE_THREADS = 1024;
+constexpr int DECIDE_PER = 8;  // tiles per thread: ntiles <= 8192
+
+__global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int ntiles, int M) {
   if (!any_flag(d.st.active, d.B)) return;
-  __shared__ float sv[4];
-  __shared__ int si[4];
+  __shared__ float sv[DECIDE_THREADS / 64];
+  __shared__ int si[DECIDE_THREADS / 64];
   const int m = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float v[DECIDE_PER];
+  int ix[DECIDE_PER];
+#pragma unroll
+  for (int q = 0; q < DECIDE_PER; ++q) {
+    const int t = threadIdx.x + q * DECIDE_THREADS;
+    v[q] = -INFINITY;
+    ix[q] = 0x7fffffff;
+    if (t < ntiles) {
+      v[q] = d.best_val[(size_t)t * M + m];
+      ix[q] = d.best_idx[(size_t)t * M + m];
+    }
+  }
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int t = threadIdx.x; t < ntiles; t += 256) {
-    const float v = d.best_val[(size_t)t * M + m];
-    const int i = d.best_idx[(size_t)t * M + m];
-    if (better(v, i, bv, bi)) { bv = v; bi = i; }
-  }
+#pragma unroll
+  for (int q = 0; q < DECIDE_PER; ++q)
+    if (better(v[q], ix[q], bv, bi)) { bv = v[q]; bi = ix[q]; }
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const float ov = __shfl_xor(bv, o, WAVE);
@@ -551,7 +565,7 @@ __global__ __launch_bounds__(256) void k_decide(DecideArgs d, int ntiles, int M)
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int q = 1; q < 4; ++q)
+    for (int q = 1; q < DECIDE_THREADS / 64; ++q)
       if (better(sv[q], si[q], bv, bi)) { bv = sv[q]; bi = si[q]; }
     decide_one(d, m, bi, d.stop_buf[m]);
   }
@@ -681,11 +695,11 @@ static void run_skinny(const GemmArgs& a, int nsplit, int tag, Stream s) {
   dim3 grid(a.N / (16 * TN), nsplit);
   if constexpr (EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_SWIGLU) {
     if (!tag) {
-      hipLaunchKernelGGL((k_gemm_skinny<T, MT, TN, EPI, 0>), grid, dim3(256), 0, s, a);
+      launch_k((k_gemm_skinny<T, MT, TN, EPI, 0>), grid, dim3(256), 0, s, a);
       return;
     }
   }
-  hipLaunchKernelGGL((k_gemm_skinny<T, MT, TN, EPI, 1>), grid, dim3(256), 0, s, a);
+  launch_k((k_gemm_skinny<T, MT, TN, EPI, 1>), grid, dim3(256), 0, s, a);
 }
 
 template <typename T, int TN, int EPI>
@@ -699,8 +713,8 @@ static void run_skinny_mt(const GemmArgs& a, int nsplit, int tag, Stream s) {
 template <typename T, int TN, int EPI, int XS>
 static void run_staged(const GemmArgs& a, int nsplit, int tag, size_t lds, Stream s) {
   dim3 grid(a.N / (16 * TN), nsplit);
-  if (!tag) hipLaunchKernelGGL((k_gemm_staged<T, TN, EPI, 0, XS>), grid, dim3(STG_THREADS), lds, s, a);
-  else hipLaunchKernelGGL((k_gemm_staged<T, TN, EPI, 1, XS>), grid, dim3(STG_THREADS), lds, s, a);
+  if (!tag) launch_k((k_gemm_staged<T, TN, EPI, 0, XS>), grid, dim3(STG_THREADS), lds, s, a);
+  else launch_k((k_gemm_staged<T, TN, EPI, 1, XS>), grid, dim3(STG_THREADS), lds, s, a);
 }
 
 // Staged launch (X built in LDS): k-split and the checks that the prologue fits.
@@ -766,7 +780,7 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
       return -1;
     } else {
       dim3 grid((a.N + 127) / 128, (a.M + 127) / 128);
-      hipLaunchKernelGGL((k_gemm_big<T, EPI>), grid, dim3(256), 0, s, a);
+      launch_k((k_gemm_big<T, EPI>), grid, dim3(256), 0, s, a);
       return 0;
     }
   }
@@ -817,7 +831,8 @@ bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split) {
 
 int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s) {
   // ntiles: argmax partials written per row by the LM-head launch
-  hipLaunchKernelGGL(k_decide, dim3(M), dim3(256), 0, s, d, ntiles, M);
+  if (ntiles > DECIDE_THREADS * DECIDE_PER) return -1;
+  launch_k(k_decide, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles, M);
   return 0;
 }
 
@@ -825,8 +840,8 @@ int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s) {
   dim3 grid(a.M);
 #define HAM_RED(EP)                                                                                     \
   do {                                                                                                  \
-    if (dtype == 1) hipLaunchKernelGGL((k_split_reduce<bf16, EP>), grid, dim3(256), 0, s, a);           \
-    else hipLaunchKernelGGL((k_split_reduce<float, EP>), grid, dim3(256), 0, s, a);                    \
+    if (dtype == 1) launch_k((k_split_reduce<bf16, EP>), grid, dim3(256), 0, s, a);           \
+    else launch_k((k_split_reduce<float, EP>), grid, dim3(256), 0, s, a);                    \
   } while (0)
   if (epi == EPI_OP) HAM_RED(EPI_OP);
   else if (epi == EPI_XMASK) HAM_RED(EPI_XMASK);

@@ -83,8 +83,8 @@ __global__ __launch_bounds__(NORM_THREADS) void k_rmsnorm(NormArgs a) {
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
   if (a.R <= 0) return 0;
   if (a.d > NORM_THREADS * NORM_MAXV) return -1;
-  if (dtype == 1) hipLaunchKernelGGL((k_rmsnorm<bf16>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
-  else hipLaunchKernelGGL((k_rmsnorm<float>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
+  if (dtype == 1) launch_k((k_rmsnorm<bf16>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
+  else launch_k((k_rmsnorm<float>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
   return 0;
 }
 
@@ -140,8 +140,8 @@ __global__ __launch_bounds__(64) void k_rope_append(RopeArgs a) {
 int launch_rope_append(int dtype, const RopeArgs& a, Stream s) {
   if (a.R <= 0) return 0;
   dim3 grid(a.H + 2 * a.Hkv, a.R);
-  if (dtype == 1) hipLaunchKernelGGL((k_rope_append<bf16>), grid, dim3(64), 0, s, a);
-  else hipLaunchKernelGGL((k_rope_append<float>), grid, dim3(64), 0, s, a);
+  if (dtype == 1) launch_k((k_rope_append<bf16>), grid, dim3(64), 0, s, a);
+  else launch_k((k_rope_append<float>), grid, dim3(64), 0, s, a);
   return 0;
 }
 
@@ -361,8 +361,8 @@ __global__ void k_fill_f32(float* p, long long n, float v) {
 // ---------------------------------------------------------------- launchers
 #define HAM_T_LAUNCH(dtype, kern, grid, block, s, arg)                           \
   do {                                                                           \
-    if ((dtype) == 1) hipLaunchKernelGGL((kern<bf16>), grid, block, 0, s, arg);  \
-    else hipLaunchKernelGGL((kern<float>), grid, block, 0, s, arg);              \
+    if ((dtype) == 1) launch_k((kern<bf16>), grid, block, 0, s, arg);  \
+    else launch_k((kern<float>), grid, block, 0, s, arg);              \
   } while (0)
 
 void launch_macro_begin(int dtype, const MacroArgs& a, Stream s) {
@@ -372,13 +372,13 @@ void launch_embed_attn(int dtype, const EmbedAttnArgs& a, Stream s) {
   HAM_T_LAUNCH(dtype, k_embed_attn, dim3(a.B, a.H), dim3(64), s, a);
 }
 void launch_prefill_begin(const PrefillArgs& a, Stream s) {
-  hipLaunchKernelGGL(k_prefill_begin, dim3((a.B + 255) / 256), dim3(256), 0, s, a);
+  launch_k(k_prefill_begin, dim3((a.B + 255) / 256), dim3(256), 0, s, a);
 }
 void launch_gather_rows(int dtype, const GatherArgs& a, Stream s) {
   HAM_T_LAUNCH(dtype, k_gather_rows, dim3(a.R), dim3(256), s, a);
 }
 void launch_copy_row(const float* src, float* dst, int d, Stream s) {
-  hipLaunchKernelGGL(k_copy_row, dim3(1), dim3(256), 0, s, src, dst, d);
+  launch_k(k_copy_row, dim3(1), dim3(256), 0, s, src, dst, d);
 }
 void launch_micro_prep(int dtype, const MicroPrepArgs& a, Stream s) {
   const int rows = a.k == 1 ? a.B * (a.C + 1) : a.B;
@@ -394,7 +394,7 @@ void launch_fill_f32(float* p, long long n, float v, Stream s) {
   long long blocks = (n + 255) / 256;
   if (blocks > 65536) blocks = 65536;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_fill_f32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  launch_k(k_fill_f32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
 }
 
 }  // namespace ham

@@ -29,10 +29,39 @@ METRIC = "output tokens/s at 1 GPU; KV entries per output token; decode HBM GB/s
 HBM_PEAK_GBS = 8000.0
 PROF_NAMES = ["qkv", "o_proj", "gate_up", "down", "micro_gemm", "embed_gemm", "lm_head_k0", "lm_head_micro",
               "attn_decode"]
-DOMINANT_KERNEL = {
-    # template arguments: element type, 16-row tiles, 16-column tiles per wave, epilogue (3 = SwiGLU), tag
-    "gate_up": "k_gemm_skinny<unsigned short, 1, 2, 3, 0> (base-layer gate/up weight streaming, SwiGLU epilogue)",
-}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gate_up_c2_1b_bf16.txt")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2505_20438_amd", "csrc", "kernels_gemm.hip")
+
+
+def gate_up_kernel(w: Workload) -> str:
+    """Profiler name of the base-layer gate/up kernel at this workload.
+
+    Batches whose normalised rows fit the staged prologue (rows * d_model <= 4096)
+    run the staged GEMM (X built in LDS; template: element type, 16-column tiles
+    per workgroup, epilogue 3 = SwiGLU, tag 0 = base layer, X source 1 = RMSNorm);
+    larger batches the plain skinny GEMM after a separate RMSNorm kernel.
+    """
+    s = w.shape
+    elem = "unsigned short" if s.dtype == BF16 else "float"
+    tn = 2 if (2 * s.ffn_dim) // 32 >= 512 else 1
+    if w.batch <= 8 and w.batch * s.d_model <= 4096:
+        return f"k_gemm_staged<{elem}, {tn}, 3, 0, 1>"
+    mt = 1 if w.batch <= 16 else (2 if w.batch <= 32 else 4)
+    return f"k_gemm_skinny<{elem}, {mt}, {tn}, 3, 0>"
+
+
+def measured_traffic(w: Workload, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None
+    when the summary is for another kernel or workload, or the GEMM source changed."""
+    import hashlib
+    try:
+        fields = dict(l.split("=", 1) for l in open(TRAFFIC_FILE).read().split("\n") if "=" in l and not l.startswith("#"))
+        src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if fields.get("kernel") != kernel or fields.get("workload") != w.name or fields.get("source_sha256") != src:
+        return None
+    return float(fields["fetch_bytes_per_launch"]) + float(fields["write_bytes_per_launch"])
 
 
 def group_lengths(sched: np.ndarray, budget: int) -> list:
@@ -46,7 +75,7 @@ def group_lengths(sched: np.ndarray, budget: int) -> list:
     return out
 
 
-def algorithmic_bytes(w: Workload, lens: list) -> float:
+def algorithmic_bytes(w: Workload, lens: list, max_steps: int = 0) -> float:
     """Bytes the decode loop must move (closed form over the realised schedule).
 
     Per macro-step s (consuming group s-1, emitting group s), while any sequence
@@ -64,6 +93,8 @@ def algorithmic_bytes(w: Workload, lens: list) -> float:
     W_emb = 5 * d * d * es
     kv_slot = s.n_layers * 2 * Hk * hd * es
     steps = max(len(l) for l in lens) - 1
+    if max_steps > 0:
+        steps = min(steps, max_steps)
     total = 0.0
     for st in range(1, steps + 1):
         run = [b for b in range(len(lens)) if st < len(lens[b])]
@@ -107,6 +138,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c2_1b_bf16", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-steps", type=int, default=3, help="macro-steps of the oracle sample (0 = skip)")
+    ap.add_argument("--max-macro-steps", type=int, default=0,
+                    help="stop each run after this many macro-steps (profiler passes only; 0 = whole workload)")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="first run one plain device-to-device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); the batch would shard "
@@ -135,6 +170,16 @@ def main() -> int:
     lens = [group_lengths(sched_np[b], w.max_new) for b in range(B)]
     n_steps = max(len(l) for l in lens) - 1
     tokens_per_run = sum(budgets)
+    if args.max_macro_steps > 0 and args.max_macro_steps < n_steps:
+        n_steps = args.max_macro_steps   # profiler passes: the JSON line is then not a benchmark result
+        tokens_per_run = sum(sum(l[:n_steps + 1]) for l in lens)
+    if args.copy_calibration_mb > 0:
+        src = torch.ones(args.copy_calibration_mb << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def one_run(profile: bool = False):
         e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
@@ -153,7 +198,6 @@ def main() -> int:
 
     for _ in range(args.warmup):
         one_run()
-    stats = rt.kv_stats()
     torch.cuda.synchronize()
     decode_ms, prefill_ms = [], []
     t0 = time.perf_counter()
@@ -164,14 +208,16 @@ def main() -> int:
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     stats = rt.kv_stats()
-    assert all(st["tokens"] == w.max_new and st["device_error"] == 0 for st in stats), stats
+    truncated = n_steps < max(len(l) for l in lens) - 1
+    assert all((truncated or st["tokens"] == w.max_new) and st["device_error"] == 0 for st in stats), stats
     gen_slots = sum(st["gen_slots"] for st in stats)
     dec_ms = float(np.mean(decode_ms))
     value = tokens_per_run / (dec_ms / 1000.0)
-    alg_bytes = algorithmic_bytes(w, lens)
+    alg_bytes = algorithmic_bytes(w, lens, n_steps)
 
-    # per-kernel-class timing: one more run with HIP events around every launch of
-    # the classes (same launch configuration, outside the timed runs above)
+    # per-kernel-class timing: one more run with HIP events attached to the
+    # dispatch of every launch of the classes (same launch configuration, outside
+    # the timed runs above; the events mark each kernel's own start and end)
     one_run(profile=True)
     prof = (ham.HamProfT * ham.HAM_PROF_KINDS)()
     ham.check(ham.load_library().ham_profile_read(rt.handle, prof, ham.HAM_PROF_KINDS))
@@ -188,8 +234,9 @@ def main() -> int:
     roofline = {"bound": "hbm", "achieved": kd["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": kd["gbs"] / HBM_PEAK_GBS, "traffic": None, "kernel": dom,
                 "bytes_per_launch": kd["bytes_per_launch"], "avg_us": kd["avg_us"]}
-    if dom == "gate_up" and s.dtype == BF16 and B <= 16 and s.ffn_dim * 2 // 32 >= 512:
-        roofline["kernel_name"] = DOMINANT_KERNEL["gate_up"]
+    if dom == "gate_up":
+        roofline["kernel_name"] = gate_up_kernel(w)
+        roofline["traffic"] = measured_traffic(w, roofline["kernel_name"])
 
     out = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,

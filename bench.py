@@ -131,6 +131,78 @@ def cpu_baseline(w: Workload, sample_steps: int) -> dict:
                       f"excluded), float64 numpy, {platform.processor() or platform.machine()}"}
 
 
+def _config(w: Workload, **over):
+    from paper_2505_20438_amd import ham
+    s = w.shape
+    kw = dict(n_layers=s.n_layers, d_model=s.d_model, n_heads=s.n_heads, n_kv_heads=s.n_kv_heads,
+              head_dim=s.head_dim, ffn_dim=s.ffn_dim, vocab=s.vocab, micro_layers=s.micro_layers,
+              max_group=s.max_group, stop_mode=s.stop_mode, stop_id=s.stop_id, dtype=s.dtype,
+              max_batch=w.batch, max_prompt=w.prompt_len, max_steps=w.max_new)
+    kw.update(over)
+    return ham.make_config(**kw)
+
+
+def base_comparator(w: Workload, prompts, warmup: int, steps: int) -> dict:
+    """The same weights decoding one token per forward (max group 1: no embedder
+    fusion, no micro steps, one KV entry per token) on the same kernels."""
+    import torch
+    from paper_2505_20438_amd import ham
+    rt = ham.HamRuntime(_config(w, max_group=1), w.seed_weights, "cuda:0")
+    B = w.batch
+    ones = torch.ones((w.max_new + 1, B), dtype=torch.int32, device=prompts.device)
+    times = []
+    for i in range(warmup + steps):
+        rt.prefill(prompts, [w.max_new] * B, ones[0])
+        e1, e2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e1.record(rt.stream)
+        for st in range(1, w.max_new):
+            rt.macro_step(ones[st])
+        e2.record(rt.stream)
+        torch.cuda.synchronize()
+        if i >= warmup:
+            times.append(e1.elapsed_time(e2))
+    stats = rt.kv_stats()
+    assert all(st["tokens"] == w.max_new and st["gen_slots"] == w.max_new - 1 for st in stats), stats
+    ms = float(np.median(times))
+    del rt
+    torch.cuda.empty_cache()
+    return {"value": B * w.max_new / (ms / 1000.0), "unit": "tokens/s", "ms_per_run": ms,
+            "kv_entries_per_output_token": (w.max_new - 1) / float(w.max_new),
+            "what": "same weights and kernels, max group 1: plain one-token-per-forward decoding"}
+
+
+def head_mode_run(w: Workload, prompts, conf: float) -> dict:
+    """Model-driven groups: the stop head's logit against ln((1-c)/c).  The
+    number of macro-steps is found by an untimed run, then one run is timed."""
+    import torch
+    from paper_2505_20438_amd import ham
+    rt = ham.HamRuntime(_config(w, stop_mode=ham.HAM_STOP_HEAD, stop_conf=conf), w.seed_weights, "cuda:0")
+    B = w.batch
+    rt.prefill(prompts, [w.max_new] * B)
+    n = 0
+    while not all(st["done"] for st in rt.kv_stats()):
+        if n >= w.max_new:  # every macro-step emits at least one token of an unfinished sequence
+            raise RuntimeError("HEAD-mode decode did not spend its budget")
+        rt.macro_step()
+        n += 1
+    rt.prefill(prompts, [w.max_new] * B)
+    e1, e2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e1.record(rt.stream)
+    for _ in range(n):
+        rt.macro_step()
+    e2.record(rt.stream)
+    torch.cuda.synchronize()
+    stats = rt.kv_stats()
+    tokens = sum(st["tokens"] for st in stats)
+    groups = sum(st["groups"] for st in stats)
+    ms = e1.elapsed_time(e2)
+    del rt
+    torch.cuda.empty_cache()
+    return {"confidence": conf, "value": tokens / (ms / 1000.0), "unit": "tokens/s", "macro_steps": n,
+            "mean_group": tokens / float(groups),
+            "kv_entries_per_output_token": sum(st["gen_slots"] for st in stats) / float(tokens)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +214,10 @@ def main() -> int:
                     help="stop each run after this many macro-steps (profiler passes only; 0 = whole workload)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run one plain device-to-device copy of this size (HBM counter calibration)")
+    ap.add_argument("--base", choices=("auto", "on", "off"), default="auto",
+                    help="also time the same model decoding one token per forward (groups of one; auto: prompts <= 4096)")
+    ap.add_argument("--head-sweep", default="",
+                    help="comma-separated confidences: also time the model-driven stop head (HEAD mode) at each")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); the batch would shard "
@@ -207,11 +283,12 @@ def main() -> int:
         decode_ms.append(dc)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    dec_med = float(np.median(decode_ms))
     stats = rt.kv_stats()
     truncated = n_steps < max(len(l) for l in lens) - 1
     assert all((truncated or st["tokens"] == w.max_new) and st["device_error"] == 0 for st in stats), stats
     gen_slots = sum(st["gen_slots"] for st in stats)
-    dec_ms = float(np.mean(decode_ms))
+    dec_ms = dec_med
     value = tokens_per_run / (dec_ms / 1000.0)
     alg_bytes = algorithmic_bytes(w, lens, n_steps)
 
@@ -246,6 +323,7 @@ def main() -> int:
                    "layers": s.n_layers, "d_model": s.d_model, "micro_layers": s.micro_layers,
                    "schedule": "forced geometric group lengths p=1/2, cap 4", "macro_steps": n_steps},
         "kv_entries_per_output_token": gen_slots / float(sum(st["tokens"] for st in stats)),
+        "kv_entries_per_token_incl_prompt": (B * P + gen_slots) / float(B * P + sum(st["tokens"] for st in stats)),
         "decode_hbm_gbs": (alg_bytes / 1e9) / (dec_ms / 1000.0),
         "decode_hbm_frac": (alg_bytes / 1e9) / (dec_ms / 1000.0) / HBM_PEAK_GBS,
         "algorithmic_bytes_per_run": alg_bytes,
@@ -255,6 +333,14 @@ def main() -> int:
         "roofline": roofline,
         "kernels": kernels,
     }
+    out["decode_ms_runs"] = [float(x) for x in decode_ms]
+    del rt
+    torch.cuda.empty_cache()
+    if args.base == "on" or (args.base == "auto" and P <= 4096 and not truncated):
+        out["base_comparator"] = base_comparator(w, prompts, args.warmup, args.steps)
+        out["speedup_vs_base"] = value / out["base_comparator"]["value"]
+    if args.head_sweep:
+        out["head_sweep"] = [head_mode_run(w, prompts, float(c)) for c in args.head_sweep.split(",")]
     if args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_steps)
     print(json.dumps(out))

@@ -168,3 +168,64 @@ def test_1b_bf16_teacher_forced_prefix(torch_cuda):
     exact, ties = _teacher_forced(om, shp, prompts, [w.max_new], steps, sched, w.seed_weights,
                                   debug_steps=steps + 1)
     assert ties <= 1
+
+
+def _free_running_compare(orc, res, tol, tau):
+    """Walk the free-running GPU groups against the oracle's until the first
+    divergence, which must be a near tie the measured error explains (of the
+    token argmax, or of the stop logit against tau).  Returns exact decisions."""
+    decs = {(d.step, d.k): d for d in orc.decisions}
+    exact = 0
+    for step, (g_gpu, g_orc) in enumerate(zip(res.groups[0], orc.groups)):
+        for k in range(min(len(g_gpu), len(g_orc))):
+            d = decs[(step, k)]
+            lg = res.logits[(0, step, k)]
+            assert np.max(np.abs(lg - d.logits)) <= tol, (step, k)
+            assert np.max(np.abs(res.hidden[(0, step, k)] - d.h)) <= tol, (step, k)
+            if g_gpu[k] != g_orc[k]:
+                check_decision(d, g_gpu[k], lg, tol)
+                return exact
+            exact += 1
+        if len(g_gpu) != len(g_orc):  # the stop test at the shorter group's last token differed
+            k = min(len(g_gpu), len(g_orc)) - 1
+            d = decs[(step, k)]
+            err = abs(res.stop[(0, step, k)] - d.stop_logit)
+            assert err <= tol and abs(d.stop_logit - tau) <= 2 * err, (step, k, d.stop_logit, err)
+            return exact
+    assert len(res.groups[0]) == len(orc.groups)
+    return exact
+
+
+def test_1b_dims_head_mode_free_running(torch_cuda):
+    # model-driven stopping (HEAD mode, c = 0.5) at the 1B layer shape and full vocabulary,
+    # two base layers and one micro layer; free-running against the free-running oracle
+    shp = dataclasses.replace(SHAPE_1B, n_layers=2, micro_layers=1, stop_mode=STOP_HEAD, stop_conf=0.5)
+    P, steps = 64, 10
+    prompts = synth.prompt_ids(4010, 1, P, shp.vocab)
+    om = OracleHam(shp, 6010)
+    orc = oracle_groups_for(om, prompts, [0], steps, None, record=True)[0]
+    rt = _runtime(shp, 6010, 1, P, steps)
+    res = run_gpu(rt, prompts, [0], steps, debug_steps=steps + 1)
+    exact = _free_running_compare(orc, res, TOL[BF16], 0.0)
+    lens = [len(g) for g in orc.groups]
+    print("oracle group lengths", lens, "exact decisions", exact)
+    assert exact >= 10
+    assert len(set(lens)) > 1  # the stop head actually varies the group length here
+
+
+def test_head_c1_equals_one_token_decoding(torch_cuda):
+    # c = 1 stops after every token: the loop reduces to plain decoding, and must give the
+    # same tokens as the same weights configured with max group 1 (the base comparator)
+    import torch
+    w = WORKLOADS["c2_1b_bf16"]
+    shp_h = dataclasses.replace(w.shape, n_layers=4, stop_mode=STOP_HEAD, stop_conf=1.0)
+    shp_1 = dataclasses.replace(w.shape, n_layers=4, max_group=1)
+    P, steps = 128, 24
+    prompts = synth.prompt_ids(4011, 2, P, shp_h.vocab)
+    res_h = run_gpu(_runtime(shp_h, 6011, 2, P, steps), prompts, [0, 0], steps)
+    sched = np.ones((2, steps + 1), dtype=np.int64)
+    res_1 = run_gpu(_runtime(shp_1, 6011, 2, P, steps), prompts, [0, 0], steps, sched)
+    for b in range(2):
+        assert all(len(g) == 1 for g in res_h.groups[b])
+        assert res_h.groups[b] == res_1.groups[b]
+        assert res_h.stats[b]["kv_len"] == res_1.stats[b]["kv_len"] == P + steps

@@ -409,7 +409,7 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
 
   // gate/up, second norm folded in
   GemmArgs gu{};
-  gu.gate = gate; gu.gate_n = gate_n; gu.M = R;
+  gu.gate = gate; gu.gate_n = gate_n; gu.M = R; gu.part = m->WS<float>(y.part);  // free again once x is normed
   gu.W = m->W<char>(y.Wgu[j]); gu.N = 2 * y.F; gu.K = y.d; gu.out = m->WS<char>(y.act); gu.ldo = y.F;
   gu.xsrc = XS_NORM;
   gu.xs.x = x; gu.xs.ldx = y.d; gu.xs.part = pend.part; gu.xs.nsplit = pend.nsplit; gu.xs.pM = pend.M;

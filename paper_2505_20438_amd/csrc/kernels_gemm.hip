@@ -98,6 +98,9 @@ __device__ __forceinline__ void skinny_mma(f4 (*acc)[TN], const SkinnyBatch<T, M
 template <typename T, int MT, int TN, int EPI, int NW>
 __device__ __forceinline__ void skinny_finish(const GemmArgs& a, f4 (*acc)[TN], float* red, int ntile, int split,
                                               int nsplit, int n0);
+template <typename T, int MT, int TN, int EPI>
+__device__ __forceinline__ void skinny_epilogue(const GemmArgs& a, f4 (*acc)[TN], int ntile, int split, int nsplit,
+                                                int n0);
 
 // TAG only separates the names of base-layer launches (always active) from the
 // others in profiler output; the code is the same.
@@ -198,6 +201,16 @@ __device__ __forceinline__ void skinny_finish(const GemmArgs& a, f4 (*acc)[TN], 
         for (int p = 0; p < NW - 1; ++p) v += red[(p * NACC + q) * 64 + lane];
         acc[i][j][r] = v;
       }
+  skinny_epilogue<T, MT, TN, EPI>(a, acc, ntile, split, nsplit, n0);
+}
+
+// Epilogue of one wave's finished accumulators (rows 16i + 4g + r, columns
+// n0 + 16j + r16): split partials, the LM head's per-tile argmax, or the fused epilogue.
+template <typename T, int MT, int TN, int EPI>
+__device__ __forceinline__ void skinny_epilogue(const GemmArgs& a, f4 (*acc)[TN], int ntile, int split, int nsplit,
+                                                int n0) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, g = lane >> 4;
   if (nsplit > 1) {  // partial of this k-chunk; the consumer sums the chunks in order
 #pragma unroll
     for (int i = 0; i < MT; ++i)
@@ -524,6 +537,114 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
   skinny_finish<T, 1, TN, EPI, STG_NW>(a, acc, red, ntile, split, nsplit, n0);
 }
 
+// ------------------------------------------------------------------------ wide
+// Batched skinny GEMM (8 < M <= 64 rows): a workgroup of eight waves owns eight
+// column tiles of 16*TN columns (one per wave) and one k-range.  The X rows of
+// the k-range pass through LDS in chunks of WIDE_KC columns shared by the eight
+// waves, so a workgroup reads X once for eight tiles instead of once per tile;
+// each wave streams its own weight blocks with the next chunk in flight.  Waves
+// own disjoint columns, so there is no cross-wave reduction.
+constexpr int WIDE_NW = 8;
+constexpr int WIDE_KC = 128;
+constexpr int MAX_WIDE_SWIGLU_SPLIT = 4;
+
+template <typename T, int MT, int TN, int EPI, int TAG>
+__global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, FPC = WIDE_KC / KB;
+  constexpr int PL = Act<T>::PL;
+  constexpr int ROWB = WIDE_KC * (int)sizeof(T) + 16;  // one row-plane of a chunk, padded against bank conflicts
+  constexpr int RT = MT * 16;
+  constexpr int PIECES = WIDE_KC * (int)sizeof(T) / 16;
+  constexpr int ITEMS = RT * PL * PIECES;
+  constexpr int IPT = (ITEMS + 64 * WIDE_NW - 1) / (64 * WIDE_NW);
+  __shared__ __align__(16) char xs[2][RT][PL][ROWB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int ntiles = a.N / (16 * TN);
+  const int ntile = blockIdx.x * WIDE_NW + w;
+  const bool tile_ok = ntile < ntiles;
+  const int n0 = ntile * 16 * TN;
+  const int split = blockIdx.y, nsplit = gridDim.y;
+  const int nfr = a.K / KB, nch = a.K / WIDE_KC;
+  const int ch0 = (int)((long)split * nch / nsplit), ch1 = (int)((long)(split + 1) * nch / nsplit);
+  const T* W = (const T*)a.W;
+  const T* X = (const T*)a.X;
+  const T* wrow[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)  // a wave past the last tile streams the last tile's blocks (never used)
+    wrow[j] = W + (size_t)((tile_ok ? ntile : ntiles - 1) * TN + j) * nfr * 64 * EPL + (size_t)lane * EPL;
+
+  u4 xr[IPT];
+  auto xload = [&](int c) {
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int i = tid + q * 64 * WIDE_NW;
+      xr[q] = zero16();
+      if (i < ITEMS) {
+        const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
+        if (m < a.M) xr[q] = ld16(X + ((size_t)m * PL + p) * a.ldx + (size_t)c * WIDE_KC + pc * (16 / (int)sizeof(T)));
+      }
+    }
+  };
+  auto xstore = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int i = tid + q * 64 * WIDE_NW;
+      if (i < ITEMS) {
+        const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
+        *reinterpret_cast<u4*>(&xs[buf][m][p][pc * 16]) = xr[q];
+      }
+    }
+  };
+  u4 wa[FPC][TN], wb[FPC][TN];
+  auto wload = [&](u4 (*dst)[TN], int c) {
+#pragma unroll
+    for (int f = 0; f < FPC; ++f)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) dst[f][j] = ld16_stream(wrow[j] + (size_t)(c * FPC + f) * 64 * EPL);
+  };
+  f4 acc[MT][TN];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  if (ch0 < ch1) {
+    xload(ch0);
+    wload(wa, ch0);
+    xstore(0);
+  }
+  __syncthreads();
+  for (int c = ch0; c < ch1; ++c) {
+    const int buf = (c - ch0) & 1;
+    const bool more = c + 1 < ch1;
+    if (more) {
+      xload(c + 1);
+      wload(wb, c + 1);
+    }
+#pragma unroll
+    for (int f = 0; f < FPC; ++f) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        const char* xp = &xs[buf][i * 16 + r16][0][(f * KB + g * EPL) * (int)sizeof(T)];
+        const u4 h = *reinterpret_cast<const u4*>(xp);
+        const u4 l = Act<T>::SPLIT ? *reinterpret_cast<const u4*>(xp + ROWB) : zero16();
+#pragma unroll
+        for (int j = 0; j < TN; ++j) mma_act<T>(acc[i][j], h, l, wa[f][j]);
+      }
+    }
+    if (more) {
+      xstore(buf ^ 1);
+#pragma unroll
+      for (int f = 0; f < FPC; ++f)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) wa[f][j] = wb[f][j];
+    }
+    __syncthreads();
+  }
+  if (tile_ok) skinny_epilogue<T, MT, TN, EPI>(a, acc, ntile, split, nsplit, n0);
+}
+
 // Final argmax of one row over all column tiles (fixed total order: larger value,
 // then lower index), then the decision and stop test of that sequence.  Each
 // thread issues all of its tile loads before comparing any of them.
@@ -572,13 +693,28 @@ __global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int nti
 }
 
 // Sum the split-K partials of a GEMM in split order and apply its epilogue.
+// SwiGLU: output feature f pairs gate column 16*(f/8) + f%8 with the up column 8 after it.
 template <typename T, int EPI>
 __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   const int m = blockIdx.x;
+  const float* pm = a.part + (size_t)m * a.N;
+  const size_t ss = (size_t)a.M * a.N;
+  if constexpr (EPI == EPI_SWIGLU) {
+    for (int f = threadIdx.x; f < a.N / 2; f += 256) {
+      const int ng = (f / 8) * 16 + f % 8;
+      float gv = 0.f, uv = 0.f;
+      for (int s = 0; s < a.nsplit; ++s) {
+        gv += pm[s * ss + ng];
+        uv += pm[s * ss + ng + 8];
+      }
+      Act<T>::put(a.out, m, a.ldo, f, gv / (1.0f + expf(-gv)) * uv);
+    }
+    return;
+  }
   for (int n = threadIdx.x; n < a.N; n += 256) {
     float v = 0.f;
-    for (int s = 0; s < a.nsplit; ++s) v += a.part[((size_t)s * a.M + m) * a.N + n];
+    for (int s = 0; s < a.nsplit; ++s) v += pm[s * ss + n];
     if constexpr (EPI == EPI_OP) {
       Act<T>::put(a.out, m, a.ldo, n, v);
     } else if constexpr (EPI == EPI_XMASK) {
@@ -787,6 +923,35 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
   const int nfr = a.K / KB;
   const int ntiles = skinny_tiles(a.N);
   const int TN = a.N / (16 * ntiles);
+  if (a.M > 8 && a.K % WIDE_KC == 0 && EPI != EPI_XMASK && EPI != EPI_OP) {
+    // batched rows: X through LDS once per workgroup of eight tiles; about 512 workgroups,
+    // split-K (SwiGLU then finishes in k_split_reduce; the argmax never splits)
+    const int groups = (ntiles + WIDE_NW - 1) / WIDE_NW;
+    const int nch = a.K / WIDE_KC;
+    int nsplit = 1;
+    if (EPI != EPI_ARGMAX && (max_split > 1 || EPI == EPI_SWIGLU))
+      nsplit = std::max(1, std::min(std::min((512 + groups - 1) / groups, nch),
+                                    EPI == EPI_SWIGLU ? MAX_WIDE_SWIGLU_SPLIT : max_split));
+    a.nsplit = nsplit;
+    *nsplit_out = EPI == EPI_SWIGLU ? 1 : nsplit;  // SwiGLU partials are finished here
+    dim3 grid(groups, nsplit);
+    const int mt = (a.M + 15) / 16;
+#define HAM_WIDE(MTV, TNV)                                                                              \
+    do {                                                                                                \
+      if (!tag && (EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_SWIGLU))                            \
+        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 0>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
+      else                                                                                              \
+        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 1>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
+    } while (0)
+    if (TN == 2) {
+      if (mt <= 2) HAM_WIDE(2, 2); else HAM_WIDE(4, 2);
+    } else {
+      if (mt <= 2) HAM_WIDE(2, 1); else HAM_WIDE(4, 1);
+    }
+#undef HAM_WIDE
+    if (EPI == EPI_SWIGLU && nsplit > 1) launch_k((k_split_reduce<T, EPI_SWIGLU>), dim3(a.M), dim3(256), 0, s, a);
+    return 0;
+  }
   int nsplit = 1;
   if (EPI != EPI_ARGMAX && EPI != EPI_SWIGLU && max_split > 1) {
     // about 1024 workgroups, at least four fragments per wave
@@ -846,6 +1011,7 @@ int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s) {
   if (epi == EPI_OP) HAM_RED(EPI_OP);
   else if (epi == EPI_XMASK) HAM_RED(EPI_XMASK);
   else if (epi == EPI_F32) HAM_RED(EPI_F32);
+  else if (epi == EPI_SWIGLU) HAM_RED(EPI_SWIGLU);
   else return -1;
 #undef HAM_RED
   return 0;

@@ -32,7 +32,9 @@ size_t ham_op_attention_workspace_bytes(int32_t rows, int32_t n_heads, int32_t n
  *  dtype        HAM_F32 or HAM_BF16 (cache element type)
  *  d_q          act rows [rows][n_heads*head_dim], RoPE already applied
  *  d_k          [rows][n_kv_heads][slots_cap][head_dim]   (slot-major)
- *  d_vt         [rows][n_kv_heads][head_dim][slots_cap]   (d-major)
+ *  d_vt         [rows][n_kv_heads][slots_cap/32][head_dim][32]   (V in 32-slot
+ *               tiles, d-major inside a tile: element (d, slot) at
+ *               ((slot/32)*head_dim + d)*32 + slot%32 of its (row, kv head))
  *  d_kv_len     int32 [rows], each <= slots_cap; d_enable int32 [rows]
  *  kv_max       host upper bound of kv_len (chooses the slot split)
  *  d_out        act rows [rows][n_heads*head_dim]

@@ -319,17 +319,17 @@ struct StepAttn {
   int kv_cap;
 };
 
-// slot splits of the fused step.  A workgroup streams its share of the cache
-// at the rate of one compute unit, so small batches spread each (row, kv head)
-// over splits of a few key blocks until about 128 workgroups run; long
-// contexts split until every wave holds at most two chunks of key blocks.
+// slot splits of the fused step.  A workgroup streams its share of the cache at
+// about the rate of one compute unit and holds one CU (its register use allows
+// one per CU), so the (row, kv head) pairs are split until about 256
+// workgroups run, keeping at least two key blocks per split; long contexts
+// then loop over chunks inside each wave rather than adding workgroups.
 int attn_step_splits(int dtype, int R, int Hk, int hd, int kv_cap) {
+  (void)hd;
   const int kb = dtype == HAM_BF16 ? 32 : 16;
   const int blocks = (kv_cap + kb - 1) / kb;
-  const int chunk = 8 * (256 / hd);  // key blocks one workgroup holds in flight
-  const int for_length = (blocks + 2 * chunk - 1) / (2 * chunk);
-  const int for_width = std::min((128 + R * Hk - 1) / (R * Hk), (blocks + 1) / 2);
-  return std::max(1, std::min(MAX_ATTN_SPLIT, std::max(for_length, for_width)));
+  const int for_width = std::min((256 + R * Hk - 1) / (R * Hk), (blocks + 1) / 2);
+  return std::max(1, std::min(MAX_ATTN_SPLIT, for_width));
 }
 
 // one transformer layer (base layer j < L, micro layer j >= L) over R rows.

@@ -26,6 +26,15 @@ inline void launch_k(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds
   }
 }
 
+// ---------------------------------------------------------------- KV cache layout
+// K [seq][kv_head][slot][hd] (slot-major).  V in tiles of VT_TILE slots, d-major
+// inside a tile: [seq][kv_head][slot / VT_TILE][hd][VT_TILE], so the values of
+// one 32-slot key block are one contiguous region, like its keys.
+constexpr int VT_TILE = 32;
+__host__ __device__ __forceinline__ size_t vt_offset(int d, int slot, int hd) {
+  return ((size_t)(slot / VT_TILE) * hd + d) * VT_TILE + slot % VT_TILE;
+}
+
 // ---------------------------------------------------------------- per-sequence state
 // Structure-of-arrays in the state buffer, each int32 [max_batch] (grp_tok, teacher:
 // [max_batch][4], hist: [max_batch][5]).
@@ -116,7 +125,7 @@ struct GemmArgs {
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
   const void* q; int ldq;          // q [R][H*hd] (storage type), RoPE applied
-  const void* K; const void* VT;   // K [b][Hkv][S][hd], VT [b][Hkv][hd][S]
+  const void* K; const void* VT;   // K [b][Hkv][S][hd], V tiled [b][Hkv][S/32][hd][32] (vt_offset)
   long long sb, sh;                // element strides per sequence and per kv head (both caches)
   int S;                           // slot capacity (row length of VT)
   int H, Hkv, hd, R, nsplit;

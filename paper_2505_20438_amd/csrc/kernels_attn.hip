@@ -1,9 +1,10 @@
 // Attention over the smashed KV cache (one slot per fused group, Sec. 3.1).
 //
-// Cache layout per layer: K [seq][kv_head][slot][hd] and V stored d-major,
-// VT [seq][kv_head][hd][slot], so that both products are matrix-core
-// contractions fed by 16-byte contiguous loads:
-//   S^T = K Q^T   (A = K rows, B = Q^T)  and  O = P V  (A = P, B = VT rows).
+// Cache layout per layer: K [seq][kv_head][slot][hd] and V in 32-slot tiles,
+// d-major inside a tile ([seq][kv_head][slot/32][hd][32], ham_internal.h), so
+// that both products are matrix-core contractions fed by 16-byte contiguous
+// loads and the K and V of a 32-slot key block are each one contiguous region:
+//   S^T = K Q^T   (A = K rows, B = Q^T)  and  O = P V  (A = P, B = V^T rows).
 // The rows of the K operand are permuted so that the score tile lands in the
 // registers exactly where the P operand of the next product needs it (lane
 // l holds the probabilities of row l & 15 for the slot slice of lane group
@@ -70,9 +71,10 @@ __device__ __forceinline__ void kv_load(KVBlock<T, HD>& blk, const T* Kb, const 
 #pragma unroll
     for (int f = 0; f < B::NF; ++f) blk.k[t][f] = ld16_stream(kp + f * KB);
   }
-  const T* vp = Vb + (size_t)r16 * S + base + g * (KB / 4);
+  // V^T row d = dt*16 + r16 of the block's tile, slots base + g*KB/4 .. (KB <= 32 stays inside one tile)
+  const T* vp = Vb + vt_offset(r16, base, HD) + g * (KB / 4);
 #pragma unroll
-  for (int dt = 0; dt < B::ND; ++dt) blk.v[dt] = ld16_stream(vp + (size_t)dt * 16 * S);
+  for (int dt = 0; dt < B::ND; ++dt) blk.v[dt] = ld16_stream(vp + (size_t)dt * 16 * VT_TILE);
 }
 
 // Keep the first `keep` elements of a lane fragment, zero the rest.
@@ -448,7 +450,7 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
     for (int d = threadIdx.x; d < HD; d += 64 * ATTN_NW) {
       const T v = from_f<T>(sraw[(grp + 1) * HD + d] * rinv);
       sh.xv[d] = to_f<T>(v);
-      ((T*)a.VT)[(size_t)r * a.sb + kvh * a.sh + (size_t)d * a.S + ri.slot] = v;
+      ((T*)a.VT)[(size_t)r * a.sb + kvh * a.sh + vt_offset(d, ri.slot, HD)] = v;
     }
   }
   // cached slots [0, cached): the first chunk is in registers already

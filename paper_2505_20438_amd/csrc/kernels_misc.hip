@@ -90,7 +90,7 @@ int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
 
 // ---------------------------------------------------------------- RoPE + KV append
 // Rotate-half RoPE of q and k at the row's position; q -> q buffer, k -> K cache
-// slot, v -> VT cache column (d-major).  One block per (head of q|k|v, row).
+// slot, v -> its column of the slot's V tile.  One block per (head of q|k|v, row).
 template <typename T>
 __global__ __launch_bounds__(64) void k_rope_append(RopeArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
@@ -130,9 +130,9 @@ __global__ __launch_bounds__(64) void k_rope_append(RopeArgs a) {
         k[i + half] = from_f<T>(y2);
       }
     } else if (ri.enabled) {
-      T* v = (T*)a.VT + ri.b * a.sb + (hh - a.H - a.Hkv) * a.sh + ri.slot;
-      v[(size_t)i * a.S] = from_f<T>(x1);
-      v[(size_t)(i + half) * a.S] = from_f<T>(x2);
+      T* v = (T*)a.VT + ri.b * a.sb + (hh - a.H - a.Hkv) * a.sh;
+      v[vt_offset(i, ri.slot, a.hd)] = from_f<T>(x1);
+      v[vt_offset(i + half, ri.slot, a.hd)] = from_f<T>(x2);
     }
   }
 }

@@ -75,7 +75,8 @@ def test_decode_attention_op(torch_cuda, case):
     dev = "cuda:0"
     Kt = torch.from_numpy(K).to(dev).to(tdt)
     Vt = torch.from_numpy(V).to(dev).to(tdt)
-    VTt = Vt.transpose(2, 3).contiguous()
+    # V in 32-slot tiles, d-major inside a tile: [R][Hk][S/32][hd][32]
+    VTt = Vt.reshape(R, Hk, S // 32, 32, hd).transpose(3, 4).contiguous()
     Kf = Kt.float().cpu().numpy()       # the stored (rounded) values both sides use
     Vf = Vt.float().cpu().numpy()
     qt = _act_rows(torch, torch.from_numpy(q).to(dev), dtype)

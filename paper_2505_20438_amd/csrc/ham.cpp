@@ -157,8 +157,9 @@ Layout make_layout(const ham_config* c) {
   y.q = take(R * y.HD * 4);
   y.ao = take(R * y.HD * 4);
   y.act = take(R * y.F * 4);
-  y.part = take((size_t)MAX_GEMM_SPLIT * 64 * y.Nmax * 4);
-  y.qpart = take((size_t)MAX_GEMM_SPLIT * 64 * y.QKV * 4);  // q/k/v partials (read while part is pending)
+  static_assert(MAX_GEMM_SPLIT * 64 <= PART_ROWS, "partial buffer rows");
+  y.part = take((size_t)PART_ROWS * y.Nmax * 4);
+  y.qpart = take((size_t)PART_ROWS * y.QKV * 4);  // q/k/v partials (read while part is pending)
   y.ssb = take((size_t)MAX_GEMM_SPLIT * 64 * 4);
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);

@@ -156,6 +156,8 @@ struct AttnStepArgs {
 typedef hipStream_t Stream;
 // tag 0: base-layer launch (distinct kernel name in profiles), 1: any other.
 // *nsplit receives the k-split used; above 1 the result is fp32 partials in a.part.
+// the split-K partial buffer holds nsplit * M <= PART_ROWS rows of N floats
+constexpr int PART_ROWS = 1024;
 // returns GEMM_NO_STAGE (nothing launched) when a staged X source does not fit
 int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, int tag, int* nsplit);
 constexpr int GEMM_NO_STAGE = -2;

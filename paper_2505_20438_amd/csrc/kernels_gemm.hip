@@ -538,7 +538,7 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------------ wide
-// Batched skinny GEMM (8 < M <= 64 rows): a workgroup of eight waves owns eight
+// Batched skinny GEMM (8 < M <= 256 rows): a workgroup of eight waves owns eight
 // column tiles of 16*TN columns (one per wave) and one k-range.  The X rows of
 // the k-range pass through LDS in chunks of WIDE_KC columns shared by the eight
 // waves, so a workgroup reads X once for eight tiles instead of once per tile;
@@ -551,11 +551,12 @@ constexpr int MAX_WIDE_SWIGLU_SPLIT = 4;
 template <typename T, int MT, int TN, int EPI, int TAG>
 __global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
-  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, FPC = WIDE_KC / KB;
+  constexpr int KC = MT <= 4 ? WIDE_KC : WIDE_KC / 2;  // k per chunk: LDS holds two chunks of all rows
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, FPC = KC / KB;
   constexpr int PL = Act<T>::PL;
-  constexpr int ROWB = WIDE_KC * (int)sizeof(T) + 16;  // one row-plane of a chunk, padded against bank conflicts
+  constexpr int ROWB = KC * (int)sizeof(T) + 16;  // one row-plane of a chunk, padded against bank conflicts
   constexpr int RT = MT * 16;
-  constexpr int PIECES = WIDE_KC * (int)sizeof(T) / 16;
+  constexpr int PIECES = KC * (int)sizeof(T) / 16;
   constexpr int ITEMS = RT * PL * PIECES;
   constexpr int IPT = (ITEMS + 64 * WIDE_NW - 1) / (64 * WIDE_NW);
   __shared__ __align__(16) char xs[2][RT][PL][ROWB];
@@ -566,7 +567,7 @@ __global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
   const bool tile_ok = ntile < ntiles;
   const int n0 = ntile * 16 * TN;
   const int split = blockIdx.y, nsplit = gridDim.y;
-  const int nfr = a.K / KB, nch = a.K / WIDE_KC;
+  const int nfr = a.K / KB, nch = a.K / KC;
   const int ch0 = (int)((long)split * nch / nsplit), ch1 = (int)((long)(split + 1) * nch / nsplit);
   const T* W = (const T*)a.W;
   const T* X = (const T*)a.X;
@@ -583,7 +584,7 @@ __global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
       xr[q] = zero16();
       if (i < ITEMS) {
         const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
-        if (m < a.M) xr[q] = ld16(X + ((size_t)m * PL + p) * a.ldx + (size_t)c * WIDE_KC + pc * (16 / (int)sizeof(T)));
+        if (m < a.M) xr[q] = ld16(X + ((size_t)m * PL + p) * a.ldx + (size_t)c * KC + pc * (16 / (int)sizeof(T)));
       }
     }
   };
@@ -898,6 +899,43 @@ static int gemm_staged(const GemmArgs& a0, int max_split, int tag, Stream s, int
   return 0;
 }
 
+// Batched rows: X through LDS once per workgroup of eight tiles; about 512
+// workgroups, split-K (SwiGLU then finishes in k_split_reduce; the argmax never splits).
+template <typename T, int EPI>
+static int gemm_wide(GemmArgs a, int max_split, int tag, Stream s, int* nsplit_out) {
+  const int ntiles = skinny_tiles(a.N);
+  const int TN = a.N / (16 * ntiles);
+
+    const int groups = (ntiles + WIDE_NW - 1) / WIDE_NW;
+    const int nch = a.K / WIDE_KC;
+    int nsplit = 1;
+    if (EPI != EPI_ARGMAX && (max_split > 1 || EPI == EPI_SWIGLU))
+      nsplit = std::max(1, std::min(std::min((512 + groups - 1) / groups, nch),
+                                    EPI == EPI_SWIGLU ? MAX_WIDE_SWIGLU_SPLIT : max_split));
+    nsplit = std::max(1, std::min(nsplit, PART_ROWS / a.M));
+    a.nsplit = nsplit;
+    *nsplit_out = EPI == EPI_SWIGLU ? 1 : nsplit;  // SwiGLU partials are finished here
+    dim3 grid(groups, nsplit);
+    const int mt = (a.M + 15) / 16;
+#define HAM_WIDE(MTV, TNV)                                                                              \
+    do {                                                                                                \
+      if (!tag && (EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_SWIGLU))                            \
+        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 0>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
+      else                                                                                              \
+        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 1>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
+    } while (0)
+    if (TN == 2) {
+      if (mt <= 2) HAM_WIDE(2, 2); else if (mt <= 4) HAM_WIDE(4, 2); else if (mt <= 8) HAM_WIDE(8, 2);
+      else if (mt <= 10) HAM_WIDE(10, 2); else HAM_WIDE(16, 2);
+    } else {
+      if (mt <= 2) HAM_WIDE(2, 1); else if (mt <= 4) HAM_WIDE(4, 1); else if (mt <= 8) HAM_WIDE(8, 1);
+      else if (mt <= 10) HAM_WIDE(10, 1); else HAM_WIDE(16, 1);
+    }
+#undef HAM_WIDE
+    if (EPI == EPI_SWIGLU && nsplit > 1) launch_k((k_split_reduce<T, EPI_SWIGLU>), dim3(a.M), dim3(256), 0, s, a);
+    return 0;
+  }
+
 template <typename T, int EPI>
 static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsplit_out, bool dry = false) {
   GemmArgs a = a0;
@@ -911,6 +949,8 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
       return GEMM_NO_STAGE;
   }
   if (dry) return GEMM_NO_STAGE;
+  if (a.M > 8 && a.M <= 256 && a.K % WIDE_KC == 0 && EPI != EPI_XMASK && EPI != EPI_OP)
+    return gemm_wide<T, EPI>(a, max_split, tag, s, nsplit_out);
   if (a.M > 64) {
     if constexpr (EPI == EPI_ARGMAX) {
       return -1;
@@ -923,35 +963,6 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
   const int nfr = a.K / KB;
   const int ntiles = skinny_tiles(a.N);
   const int TN = a.N / (16 * ntiles);
-  if (a.M > 8 && a.K % WIDE_KC == 0 && EPI != EPI_XMASK && EPI != EPI_OP) {
-    // batched rows: X through LDS once per workgroup of eight tiles; about 512 workgroups,
-    // split-K (SwiGLU then finishes in k_split_reduce; the argmax never splits)
-    const int groups = (ntiles + WIDE_NW - 1) / WIDE_NW;
-    const int nch = a.K / WIDE_KC;
-    int nsplit = 1;
-    if (EPI != EPI_ARGMAX && (max_split > 1 || EPI == EPI_SWIGLU))
-      nsplit = std::max(1, std::min(std::min((512 + groups - 1) / groups, nch),
-                                    EPI == EPI_SWIGLU ? MAX_WIDE_SWIGLU_SPLIT : max_split));
-    a.nsplit = nsplit;
-    *nsplit_out = EPI == EPI_SWIGLU ? 1 : nsplit;  // SwiGLU partials are finished here
-    dim3 grid(groups, nsplit);
-    const int mt = (a.M + 15) / 16;
-#define HAM_WIDE(MTV, TNV)                                                                              \
-    do {                                                                                                \
-      if (!tag && (EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_SWIGLU))                            \
-        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 0>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
-      else                                                                                              \
-        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 1>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
-    } while (0)
-    if (TN == 2) {
-      if (mt <= 2) HAM_WIDE(2, 2); else HAM_WIDE(4, 2);
-    } else {
-      if (mt <= 2) HAM_WIDE(2, 1); else HAM_WIDE(4, 1);
-    }
-#undef HAM_WIDE
-    if (EPI == EPI_SWIGLU && nsplit > 1) launch_k((k_split_reduce<T, EPI_SWIGLU>), dim3(a.M), dim3(256), 0, s, a);
-    return 0;
-  }
   int nsplit = 1;
   if (EPI != EPI_ARGMAX && EPI != EPI_SWIGLU && max_split > 1) {
     // about 1024 workgroups, at least four fragments per wave

@@ -101,6 +101,28 @@ __device__ __forceinline__ u4 ld16_stream(const void* p) {
 }
 __device__ __forceinline__ u4 zero16() { return u4{0u, 0u, 0u, 0u}; }
 
+// Raw buffer loads with the hardware range check: a lane whose byte offset lies
+// at or past the descriptor's size gets zeros and makes no memory request.  A
+// loop of such loads stays free of branches (the compiler can then wait for
+// just the loads it needs) without fetching anything for its idle lanes.
+// Descriptor word 3 is the gfx9-family default (no format conversion); the
+// base must be wave-uniform.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+constexpr uint32_t BUF_OOB = 0xFFFFFFF0u;
+__device__ __forceinline__ BufRsrc buf_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ f4 buf_f4(BufRsrc r, uint32_t off) {
+  return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float buf_f1(BufRsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+// streamed (non-temporal) 16-byte load
+__device__ __forceinline__ u4 buf_u4_stream(BufRsrc r, uint32_t off) {
+  return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
+}
+
 // pack 8 floats (bf16) / 4 floats (fp32) into one lane fragment
 __device__ __forceinline__ u4 pack_frag_bf16(const float* v) {
   u4 r;

@@ -18,6 +18,7 @@
 // accumulator's columns are output features: lane l holds column l & 15 of a
 // 16-column tile for rows 4*(l >> 4) + i.
 #include <algorithm>
+#include <type_traits>
 
 #include "decide.h"
 #include "device_common.h"
@@ -75,11 +76,13 @@ __device__ __forceinline__ void skinny_load(SkinnyBatch<T, MT, TN>& b, const T* 
     for (int j = 0; j < TN; ++j) b.w[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * 64 * EPL);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const u4 h = ld16(xrow[i] + (size_t)(f + u) * KB);
-      b.xh[u][i] = xok[i] ? h : zero16();
-      if constexpr (Act<T>::SPLIT) {
-        const u4 l = ld16(xrow[i] + lo_off + (size_t)(f + u) * KB);
-        b.xl[u][i] = xok[i] ? l : zero16();
+      // only lanes of live rows load (rows past M would fetch 1 KB per wave
+      // instruction through the vector cache for nothing)
+      b.xh[u][i] = zero16();
+      b.xl[u][i] = zero16();
+      if (xok[i]) {
+        b.xh[u][i] = ld16(xrow[i] + (size_t)(f + u) * KB);
+        if constexpr (Act<T>::SPLIT) b.xl[u][i] = ld16(xrow[i] + lo_off + (size_t)(f + u) * KB);
       }
     }
   }
@@ -158,10 +161,11 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
     for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * 64 * EPL);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      u4 h = ld16(xrow[i] + (size_t)f * KB), l = zero16();
-      if constexpr (Act<T>::SPLIT) l = ld16(xrow[i] + lo_off + (size_t)f * KB);
-      h = xok[i] ? h : zero16();
-      l = xok[i] ? l : zero16();
+      u4 h = zero16(), l = zero16();
+      if (xok[i]) {
+        h = ld16(xrow[i] + (size_t)f * KB);
+        if constexpr (Act<T>::SPLIT) l = ld16(xrow[i] + lo_off + (size_t)f * KB);
+      }
 #pragma unroll
       for (int j = 0; j < TN; ++j) mma_act<T>(acc[i][j], h, l, bw[j]);
     }
@@ -310,28 +314,45 @@ __device__ __forceinline__ void stage_put4<float>(char* stg, int Kr, int m, int 
 
 // XS_NORM prologue.  Chunk i (of M * Kr/4) is row i / (Kr/4), columns k0 + 4*(i % (Kr/4)).
 // aux: [nch] chunk sums of squares, then [M] row sums.
-template <typename T>
-__device__ __forceinline__ void stage_norm(const GemmArgs& a, char* stg, float* aux, int k0, int Kr, int split,
-                                           bool tile0) {
-  const XStage& s = a.xs;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int M = a.M, cpr = Kr / 4, nch = M * cpr;
-  const int ns = s.part ? s.nsplit : 0;
-  const bool whole = gridDim.y == 1;  // the workgroup sees whole rows: apply rinv here
+// The prologue's global loads come first in the kernel, ahead of the first
+// weight blocks: loads of one wave return in issue order, so prologue data
+// issued after the weights would wait for them.
+struct NormLoads {
   f4 v[STG_CH], gv[STG_CH];
   f4 pv[STG_CH][STG_SMAX];
+};
+__device__ __forceinline__ void stage_norm_load(const GemmArgs& a, NormLoads& L, int k0, int Kr) {
+  const XStage& s = a.xs;
+  const int tid = threadIdx.x;
+  const int M = a.M, cpr = Kr / 4, nch = M * cpr;
+  const int ns = s.part ? s.nsplit : 0;
+  // only the needed loads issue (every vector memory instruction costs address
+  // cycles for its active lanes, whether or not it fetches anything)
 #pragma unroll
   for (int j = 0; j < STG_CH; ++j) {
     const int i = tid + j * STG_THREADS;
     if (i < nch) {
       const int m = i / cpr, k = k0 + (i % cpr) * 4;
-      v[j] = *reinterpret_cast<const f4*>(s.x + (size_t)m * s.ldx + k);
-      gv[j] = *reinterpret_cast<const f4*>(s.g + k);
+      L.v[j] = *reinterpret_cast<const f4*>(s.x + (size_t)m * s.ldx + k);
+      L.gv[j] = *reinterpret_cast<const f4*>(s.g + k);
 #pragma unroll
       for (int q = 0; q < STG_SMAX; ++q)
-        if (q < ns) pv[j][q] = *reinterpret_cast<const f4*>(s.part + ((size_t)q * s.pM + m) * s.ldx + k);
+        if (q < ns) L.pv[j][q] = *reinterpret_cast<const f4*>(s.part + ((size_t)q * s.pM + m) * s.ldx + k);
     }
   }
+}
+
+template <typename T>
+__device__ __forceinline__ void stage_norm(const GemmArgs& a, NormLoads& L, char* stg, float* aux, int k0, int Kr,
+                                           int split, bool tile0) {
+  const XStage& s = a.xs;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int M = a.M, cpr = Kr / 4, nch = M * cpr;
+  const int ns = s.part ? s.nsplit : 0;
+  const bool whole = gridDim.y == 1;  // the workgroup sees whole rows: apply rinv here
+  f4* v = L.v;
+  f4* gv = L.gv;
+  f4 (*pv)[STG_SMAX] = L.pv;
   float* sq = aux;
   float* ssr = aux + nch;
 #pragma unroll
@@ -375,8 +396,40 @@ __device__ __forceinline__ void stage_norm(const GemmArgs& a, char* stg, float* 
 // s), then thread (chunk c, group sg) sums the weighted outputs of splits sg,
 // sg + SG, ... and the groups are added in order.  aux: [M][nh][ans] weights,
 // then [SG][nch] 4-value partial sums.
+struct AttnLoads {
+  f4 o[STG_AMAX];   // the split outputs this thread combines
+  float ms0, ls0;   // (max, sum) of split `lane` for this wave's first (row, head)
+};
+__device__ __forceinline__ void stage_attn_load(const GemmArgs& a, AttnLoads& L, int k0, int Kr) {
+  const XStage& s = a.xs;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int M = a.M, hd = s.hd, ans = s.ans, grp = s.grp, Hkv = s.Hkv;
+  const int h0 = k0 / hd, nh = (k0 + Kr - 1) / hd + 1 - h0;
+  const int cpr = Kr / 4, nch = M * cpr;
+  const int SG = max(1, min(STG_THREADS / nch, ans));
+  const int c = tid % nch, sg = tid / nch;
+  const bool act = tid < nch * SG;
+  const int m = c / cpr, k = k0 + (c % cpr) * 4, h = k / hd, d = k % hd;
+  if (act) {
+    const float* ob = s.rec_o + ((((size_t)m * Hkv + h / grp) * ans) * grp + h % grp) * hd + d;
+#pragma unroll
+    for (int q = 0; q < STG_AMAX; ++q) {
+      const int sp = sg + q * SG;
+      if (sp < ans) L.o[q] = *reinterpret_cast<const f4*>(ob + (size_t)sp * grp * hd);
+    }
+  }
+  L.ms0 = -INFINITY;
+  L.ls0 = 0.f;
+  if (w < M * nh && lane < ans) {
+    const int gm = w / nh, gh = h0 + w % nh;
+    const size_t q = (((size_t)gm * Hkv + gh / grp) * ans + lane) * grp + gh % grp;
+    L.ms0 = s.rec_ml[2 * q];
+    L.ls0 = s.rec_ml[2 * q + 1];
+  }
+}
+
 template <typename T>
-__device__ __forceinline__ void stage_attn(const GemmArgs& a, char* stg, float* aux, int k0, int Kr) {
+__device__ __forceinline__ void stage_attn(const GemmArgs& a, AttnLoads& L, char* stg, float* aux, int k0, int Kr) {
   const XStage& s = a.xs;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int M = a.M, hd = s.hd, ans = s.ans, grp = s.grp, Hkv = s.Hkv;
@@ -385,23 +438,19 @@ __device__ __forceinline__ void stage_attn(const GemmArgs& a, char* stg, float* 
   const int SG = max(1, min(STG_THREADS / nch, ans));
   float* wts = aux;
   f4* ps = reinterpret_cast<f4*>(aux + ((M * nh * ans + 3) & ~3));
-  // the outputs this thread combines, in flight while the weights are formed
   const int c = tid % nch, sg = tid / nch;
   const bool act = tid < nch * SG;
   const int m = c / cpr, k = k0 + (c % cpr) * 4, h = k / hd, d = k % hd;
-  f4 o[STG_AMAX];
-  if (act) {
-    const float* ob = s.rec_o + ((((size_t)m * Hkv + h / grp) * ans) * grp + h % grp) * hd + d;
-#pragma unroll
-    for (int q = 0; q < STG_AMAX; ++q) {
-      const int sp = sg + q * SG;
-      if (sp < ans) o[q] = *reinterpret_cast<const f4*>(ob + (size_t)sp * grp * hd);
-    }
-  }
+  f4* o = L.o;
   for (int gi = w; gi < M * nh; gi += STG_NW) {
     const int gm = gi / nh, gh = h0 + gi % nh;
     float ms = -INFINITY, ls = 0.f;
-    if (lane < ans) {
+    if (gi == w) {
+      if (lane < ans) {
+        ms = L.ms0;
+        ls = L.ls0;
+      }
+    } else if (lane < ans) {
       const size_t q = (((size_t)gm * Hkv + gh / grp) * ans + lane) * grp + gh % grp;
       ms = s.rec_ml[2 * q];
       ls = s.rec_ml[2 * q + 1];
@@ -465,21 +514,30 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
   const T* wrow[TN];
 #pragma unroll
   for (int j = 0; j < TN; ++j) wrow[j] = W + (size_t)(n0 / 16 + j) * nfr * 64 * EPL + (size_t)lane * EPL;
-  // the wave's first PF weight fragments are in flight before the prologue starts
-  // (8 blocks in all: more would cost the occupancy of two workgroups per CU)
+  // the prologue's loads, then the wave's first PF weight fragments, are in
+  // flight before the prologue computes (8 weight blocks in all: more would
+  // cost the occupancy of two workgroups per CU)
+  typename std::conditional<XS == XS_NORM, NormLoads, AttnLoads>::type pl;
+  if constexpr (XS == XS_NORM) stage_norm_load(a, pl, c0 * KB, Kr);
+  else stage_attn_load(a, pl, c0 * KB, Kr);
+  __builtin_amdgcn_sched_barrier(0);
   constexpr int PF = 8 / TN;
   const int npf = min(PF, f1 - f0);
   u4 wp[PF][TN];
+  {  // range-checked: blocks past this wave's k-range read zeros, fetch nothing
+    const BufRsrc rw = buf_rsrc(W, (uint32_t)((size_t)a.N * a.K * sizeof(T)));
 #pragma unroll
-  for (int u = 0; u < PF; ++u)
-    if (u < npf) {
+    for (int u = 0; u < PF; ++u)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) wp[u][j] = ld16_stream(wrow[j] + (size_t)(f0 + u) * 64 * EPL);
-    }
-  if constexpr (XS == XS_NORM) stage_norm<T>(a, stg, aux, c0 * KB, Kr, split, ntile == 0);
-  else stage_attn<T>(a, stg, aux, c0 * KB, Kr);
+      for (int j = 0; j < TN; ++j)
+        wp[u][j] = buf_u4_stream(rw, u < npf ? (uint32_t)(((size_t)(n0 / 16 + j) * nfr + f0 + u) * 64 * EPL +
+                                                          (size_t)lane * EPL) * (uint32_t)sizeof(T)
+                                             : BUF_OOB);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (XS == XS_NORM) stage_norm<T>(a, pl, stg, aux, c0 * KB, Kr, split, ntile == 0);
+  else stage_attn<T>(a, pl, stg, aux, c0 * KB, Kr);
   __syncthreads();
-  // the rest in batches of U, the first batch issued before the prefetched ones are used
   const int fr0 = f0 + npf;
   const int nb = (f1 - fr0) / U;
   u4 wc[U][TN], wn[U][TN];
@@ -489,8 +547,6 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) dst[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * 64 * EPL);
   };
-  if (nb > 0) wload(wc, fr0);
-
   const bool xrow = r16 < a.M;
   const char* xb = stg + (size_t)(xrow ? r16 : 0) * 4 * Kr + (size_t)g * EPL * sizeof(T);
   auto xfrag = [&](int f, u4& h, u4& l) {
@@ -509,6 +565,9 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, wp[u][j]);
     }
+  // the rest in batches of U; issuing the first batch only once the prefetched
+  // blocks have arrived measured faster than issuing it right after the prologue
+  if (nb > 0) wload(wc, fr0);
   for (int it = 0; it < nb; ++it) {
     const bool more = it + 1 < nb;
     if (more) wload(wn, fr0 + (it + 1) * U);

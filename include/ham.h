@@ -134,6 +134,34 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
 int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_teacher,
                    int32_t* d_out_tokens, int32_t* d_out_lens);
 
+/* Test and diagnostics: prefill from caller-given base-model inputs instead of
+ * prompt token ids (Sec. 3.1-3.2: a macro-step's base input is one fused vector
+ * at the position of its group's last token).  Input t of sequence b is the fp32
+ * vector d_embeds [batch][n_inputs][d_model] at RoPE position d_positions int32
+ * [batch][n_inputs] (each in [0, max_prompt + 4*(max_steps+1) + 8); checked on
+ * device: device_error bit 1).  One causal forward writes KV slots
+ * 0..n_inputs-1 (slot order = causal order, whatever the positions), then the
+ * first decision and micro loop emit a group; the other arguments are as in
+ * ham_prefill.  Fed the recorded inputs of a generation (the prompt tokens'
+ * embeddings at 0..P-1, then each macro-step's fused input at its position),
+ * this is the full-sequence forward that the incremental macro-steps must
+ * reproduce slot for slot.  Later ham_macro_step calls continue from position
+ * d_positions[b][n_inputs-1].  HAM_EINVAL on null pointers, HAM_ECAP if
+ * n_inputs > max_prompt + max_steps; later macro-steps return HAM_ECAP once
+ * the KV slot capacity is spent. */
+int ham_prefill_embeds(ham_model* m, int32_t batch, const float* d_embeds, const int32_t* d_positions,
+                       int32_t n_inputs, const int32_t* h_max_new, const int32_t* d_forced_lens,
+                       const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens);
+
+/* Where the smashed KV cache of base layer `layer` lives in the state buffer
+ * (one entry per base input, Sec. 3.1), in the model's storage type, with
+ * S = *slots entries of capacity per sequence:
+ *   K at *k_offset: [max_batch][n_kv_heads][S][head_dim];
+ *   V at *v_offset: 32-entry tiles, element (b, h, s, i) at
+ *     ((b*n_kv_heads + h)*(S/32) + s/32)*head_dim*32 + i*32 + s%32.
+ * HAM_EINVAL for an invalid configuration or layer. */
+int ham_state_info(const ham_config* cfg, int32_t layer, size_t* k_offset, size_t* v_offset, int32_t* slots);
+
 /* Synchronise the stream and copy the counters of each sequence of the current
  * batch into h_out[batch].  HAM_ESTATE before ham_prefill. */
 int ham_kv_stats(ham_model* m, ham_kv_stats_t* h_out);

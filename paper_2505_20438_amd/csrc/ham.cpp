@@ -570,6 +570,17 @@ size_t ham_weights_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_l
 size_t ham_state_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_layout(c).st_bytes; }
 size_t ham_workspace_bytes(const ham_config* c) { return check_cfg(c) ? 0 : make_layout(c).ws_bytes; }
 
+int ham_state_info(const ham_config* c, int32_t layer, size_t* k_offset, size_t* v_offset, int32_t* slots) {
+  if (!k_offset || !v_offset || !slots) return fail(HAM_EINVAL, "null output");
+  if (const char* e = check_cfg(c)) return fail(HAM_EINVAL, "%s", e);
+  const Layout y = make_layout(c);
+  if (layer < 0 || layer >= y.L) return fail(HAM_EINVAL, "layer %d out of range", layer);
+  *k_offset = y.Kc + (size_t)layer * y.kv_layer;
+  *v_offset = y.VTc + (size_t)layer * y.kv_layer;
+  *slots = y.S;
+  return HAM_OK;
+}
+
 int ham_tensor_info(const ham_config* c, int32_t id, size_t* offset, int32_t* rows, int32_t* cols,
                     int32_t* row_off, int32_t* mat_rows, int32_t* interleave, int32_t* tiled) {
   if (const char* e = check_cfg(c)) return fail(HAM_EINVAL, "%s", e);
@@ -689,14 +700,17 @@ int ham_init_weights(const ham_config* c, uint64_t seed, void* d_weights, size_t
   return HAM_OK;
 }
 
-int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t prompt_len, const int32_t* h_max_new,
-                const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens) {
-  if (!m) return fail(HAM_EINVAL, "null model");
+}  // extern "C"
+
+namespace {
+
+// Prefill of `batch` sequences of T base inputs each: prompt token ids (gathered
+// from E, positions 0..T-1), or caller-given fp32 input vectors at caller-given
+// positions.  One KV slot per input, then the first decision and micro loop.
+int prefill_common(ham_model* m, int32_t batch, int32_t T, const int32_t* d_prompt, const float* d_embeds,
+                   const int32_t* d_positions, const int32_t* h_max_new, const int32_t* d_forced_lens,
+                   const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens) {
   const Layout& y = m->y;
-  if (batch < 1 || prompt_len < 1 || !d_prompt || !h_max_new || !d_out_tokens || !d_out_lens)
-    return fail(HAM_EINVAL, "bad prefill arguments");
-  if (batch > y.B || prompt_len > y.P)
-    return fail(HAM_ECAP, "batch %d / prompt %d exceed capacity %d / %d", batch, prompt_len, y.B, y.P);
   if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
   if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
   for (int b = 0; b < batch; ++b)
@@ -704,14 +718,15 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
   m->batch = batch;
-  m->prompt_len = prompt_len;
+  m->prompt_len = T;
   m->steps_done = -1;
   m->has_teacher = d_teacher != nullptr;
   // budgets are read by kernels of earlier calls: let those finish, then copy synchronously
   HIP_TRY(hipStreamSynchronize(s));
   HIP_TRY(hipMemcpy(m->sp.budget, h_max_new, sizeof(int32_t) * batch, hipMemcpyHostToDevice));
   PrefillArgs pa{};
-  pa.st = m->sp; pa.B = batch; pa.P = prompt_len; pa.G = y.G; pa.forced_in = d_forced_lens;
+  pa.st = m->sp; pa.B = batch; pa.P = T; pa.G = y.G; pa.forced_in = d_forced_lens;
+  pa.pos_in = d_positions; pa.ldpos = T;
   pa.teacher_in = d_teacher; pa.out_tokens = d_out_tokens; pa.out_lens = d_out_lens;
   launch_prefill_begin(pa, s);
   float* xp = m->WS<float>(y.xp);
@@ -719,15 +734,17 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
   float* ctx = m->WS<float>(y.ctx);
   const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
   for (int b = 0; b < batch; ++b) {
-    for (int t0 = 0; t0 < prompt_len; t0 += y.Tc) {
-      const int R = std::min(y.Tc, prompt_len - t0);
-      const bool last = t0 + R == prompt_len;
+    for (int t0 = 0; t0 < T; t0 += y.Tc) {
+      const int R = std::min(y.Tc, T - t0);
+      const bool last = t0 + R == T;
       GatherArgs g{};
-      g.ids = d_prompt + (size_t)b * prompt_len + t0; g.R = R; g.E = m->W<char>(y.E); g.d = y.d; g.V = y.V;
+      if (d_embeds) g.rows = d_embeds + ((size_t)b * T + t0) * y.d;
+      else g.ids = d_prompt + (size_t)b * T + t0;
+      g.R = R; g.E = m->W<char>(y.E); g.d = y.d; g.V = y.V;
       g.x = xp; g.ldx = y.d; g.err = m->sp.err + b;
       launch_gather_rows(dt, g, s);
       RowMap rm{};
-      rm.mode = ROWS_PREFILL; rm.b = b; rm.t0 = t0; rm.st = m->sp;
+      rm.mode = ROWS_PREFILL; rm.b = b; rm.t0 = t0; rm.pos = d_positions; rm.ldpos = T; rm.st = m->sp;
       for (int l = 0; l < y.L; ++l) {
         Pending none;
         int rc = run_layer(m, l, R, rm, xp, true, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer,
@@ -749,6 +766,35 @@ int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t pr
   return HAM_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int ham_prefill(ham_model* m, int32_t batch, const int32_t* d_prompt, int32_t prompt_len, const int32_t* h_max_new,
+                const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  const Layout& y = m->y;
+  if (batch < 1 || prompt_len < 1 || !d_prompt || !h_max_new || !d_out_tokens || !d_out_lens)
+    return fail(HAM_EINVAL, "bad prefill arguments");
+  if (batch > y.B || prompt_len > y.P)
+    return fail(HAM_ECAP, "batch %d / prompt %d exceed capacity %d / %d", batch, prompt_len, y.B, y.P);
+  return prefill_common(m, batch, prompt_len, d_prompt, nullptr, nullptr, h_max_new, d_forced_lens, d_teacher,
+                        d_out_tokens, d_out_lens);
+}
+
+int ham_prefill_embeds(ham_model* m, int32_t batch, const float* d_embeds, const int32_t* d_positions,
+                       int32_t n_inputs, const int32_t* h_max_new, const int32_t* d_forced_lens,
+                       const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  const Layout& y = m->y;
+  if (batch < 1 || n_inputs < 1 || !d_embeds || !d_positions || !h_max_new || !d_out_tokens || !d_out_lens)
+    return fail(HAM_EINVAL, "bad prefill arguments");
+  if (batch > y.B || n_inputs > y.P + y.steps)
+    return fail(HAM_ECAP, "batch %d / inputs %d exceed capacity %d / %d", batch, n_inputs, y.B, y.P + y.steps);
+  return prefill_common(m, batch, n_inputs, nullptr, d_embeds, d_positions, h_max_new, d_forced_lens, d_teacher,
+                        d_out_tokens, d_out_lens);
+}
+
 int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens,
                    int32_t* d_out_lens) {
   if (!m) return fail(HAM_EINVAL, "null model");
@@ -756,6 +802,8 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   if (!d_out_tokens || !d_out_lens) return fail(HAM_EINVAL, "null output");
   const Layout& y = m->y;
   if (m->steps_done >= y.steps) return fail(HAM_ECAP, "max_steps (%d) reached", y.steps);
+  if (m->prompt_len + m->steps_done + 1 > y.S)
+    return fail(HAM_ECAP, "KV slot capacity (%d) reached", y.S);
   if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
   if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
   const int dt = dtype_of(m);

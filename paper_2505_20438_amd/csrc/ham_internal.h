@@ -63,7 +63,8 @@ enum RowMode { ROWS_PREFILL = 0, ROWS_DECODE = 1, ROWS_MICRO1 = 2, ROWS_MICROK =
 struct RowMap {
   int mode;
   int b;        // PREFILL: the sequence
-  int t0;       // PREFILL: slot/position of row 0
+  int t0;       // PREFILL: slot of row 0
+  const int* pos; int ldpos;  // PREFILL: RoPE position of slot t at pos[b*ldpos + t] (null: position = slot)
   int C;        // MICRO*: context rows
   int k;        // MICROK: micro step index (>= 2)
   SeqPtrs st;

@@ -28,12 +28,14 @@ struct EmbedAttnArgs {
 struct PrefillArgs {
   SeqPtrs st;
   int B, P, G;
+  const int* pos_in; int ldpos;     // [B][ldpos] positions of the P inputs, or null (0..P-1)
   const int* forced_in; const int* teacher_in;
   int* out_tokens; int* out_lens;
 };
 
 struct GatherArgs {
   const int* ids; int R; const void* E; int d, V; float* x; int ldx;
+  const float* rows;                // if set: copy fp32 rows [R][d] from here instead of gathering E rows
   int* err;                         // set (bit 2) if an id is out of range
 };
 

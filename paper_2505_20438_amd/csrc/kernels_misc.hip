@@ -268,9 +268,10 @@ __global__ void k_prefill_begin(PrefillArgs a) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= a.B) return;
   const SeqPtrs& st = a.st;
+  const int plast = a.pos_in ? a.pos_in[(size_t)b * a.ldpos + a.P - 1] : a.P - 1;
   st.kv_len[b] = a.P;
-  st.pos_last[b] = a.P - 1;
-  st.cur_pos[b] = a.P - 1;
+  st.pos_last[b] = plast;
+  st.cur_pos[b] = plast;
   st.cur_slot[b] = a.P - 1;
   st.emitted[b] = 0;
   st.done[b] = 0;
@@ -292,6 +293,10 @@ __global__ void k_prefill_begin(PrefillArgs a) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_gather_rows(GatherArgs a) {
   const int r = blockIdx.x;
+  if (a.rows) {
+    for (int i = threadIdx.x; i < a.d; i += 256) a.x[(size_t)r * a.ldx + i] = a.rows[(size_t)r * a.d + i];
+    return;
+  }
   int t = a.ids[r];
   if (t < 0 || t >= a.V) {  // caller-provided id out of range: flag it, read row 0
     if (threadIdx.x == 0) atomicOr(a.err, 2);

@@ -12,10 +12,10 @@ struct RowInfo {
 __device__ __forceinline__ RowInfo row_info(const RowMap& rm, int r) {
   RowInfo ri;
   switch (rm.mode) {
-    case ROWS_PREFILL:  // prompt tokens: one slot each, position = slot, causal
+    case ROWS_PREFILL:  // one slot per input row, causal; position = slot unless given
       ri.b = rm.b;
       ri.slot = rm.t0 + r;
-      ri.pos = ri.slot;
+      ri.pos = rm.pos ? rm.pos[(size_t)rm.b * rm.ldpos + ri.slot] : ri.slot;
       ri.n_valid = ri.slot + 1;
       ri.enabled = 1;
       break;

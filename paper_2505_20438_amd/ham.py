@@ -20,7 +20,7 @@ HAM_STOP_HEAD, HAM_STOP_TOKEN, HAM_STOP_FORCED = 0, 1, 2
 HAM_PROF_KINDS = 9
 
 EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
-            "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
+            "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
             "ham_tensor_info", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
             "ham_op_attention_workspace_bytes", "ham_op_decode_attention")
 
@@ -73,6 +73,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         getattr(lib, n).restype = SZ
     lib.ham_init_weights.argtypes = [cfgp, U64, P, SZ, P, SZ, P, SZ, P, ctypes.POINTER(P)]
     lib.ham_prefill.argtypes = [P, I32, P, I32, P, P, P, P, P]
+    lib.ham_prefill_embeds.argtypes = [P, I32, P, P, I32, P, P, P, P, P]
+    lib.ham_state_info.argtypes = [cfgp, I32, ctypes.POINTER(SZ), ctypes.POINTER(SZ), ctypes.POINTER(I32)]
     lib.ham_macro_step.argtypes = [P, P, P, P, P]
     lib.ham_kv_stats.argtypes = [P, ctypes.POINTER(HamKvStats)]
     lib.ham_set_debug.argtypes = [P, P, SZ]
@@ -87,7 +89,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_last_error.restype = ctypes.c_char_p
     lib.ham_destroy.argtypes = [P]
     lib.ham_destroy.restype = None
-    for n in ("ham_init_weights", "ham_prefill", "ham_macro_step", "ham_kv_stats", "ham_set_debug",
+    for n in ("ham_init_weights", "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug",
               "ham_steps_done", "ham_tensor_info", "ham_profile", "ham_profile_read"):
         getattr(lib, n).restype = I32
     _lib = lib
@@ -155,6 +157,22 @@ def ham_prefill(model: int, batch: int, prompt, prompt_len: int, max_new: Sequen
                                       _ptr(out_tokens), _ptr(out_lens)))
 
 
+def ham_prefill_embeds(model: int, embeds, positions, max_new: Sequence[int], forced=None, teacher=None,
+                       out_tokens=None, out_lens=None) -> None:
+    """embeds: fp32 [batch][n][d_model], positions: int32 [batch][n] (device tensors)."""
+    batch, n = int(embeds.shape[0]), int(embeds.shape[1])
+    arr = (ctypes.c_int32 * batch)(*[int(x) for x in max_new])
+    _check(load_library().ham_prefill_embeds(model, batch, _ptr(embeds), _ptr(positions), n, arr, _ptr(forced),
+                                             _ptr(teacher), _ptr(out_tokens), _ptr(out_lens)))
+
+
+def ham_state_info(cfg: HamConfig, layer: int) -> dict:
+    k, v, s = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_int32()
+    _check(load_library().ham_state_info(ctypes.byref(cfg), layer, ctypes.byref(k), ctypes.byref(v),
+                                         ctypes.byref(s)))
+    return {"k_offset": k.value, "v_offset": v.value, "slots": s.value}
+
+
 def ham_macro_step(model: int, forced=None, teacher=None, out_tokens=None, out_lens=None) -> None:
     _check(load_library().ham_macro_step(model, _ptr(forced), _ptr(teacher), _ptr(out_tokens), _ptr(out_lens)))
 
@@ -218,6 +236,29 @@ class HamRuntime:
         self.batch = prompt.shape[0]
         ham_prefill(self.handle, prompt.shape[0], prompt, prompt.shape[1], max_new, forced, teacher,
                     self.out_tokens, self.out_lens)
+
+    def prefill_embeds(self, embeds, positions, max_new, forced=None, teacher=None):
+        self.batch = embeds.shape[0]
+        ham_prefill_embeds(self.handle, embeds, positions, max_new, forced, teacher, self.out_tokens, self.out_lens)
+
+    def kv_cache(self, layer: int, n_slots: int):
+        """K and V of base layer ``layer``, slots [0, n_slots) of the current batch, as
+        float32 [batch][n_kv_heads][n_slots][head_dim] tensors (a copy)."""
+        torch = self.torch
+        info = ham_state_info(self.cfg, layer)
+        c = self.cfg
+        es = 2 if c.dtype == HAM_BF16 else 4
+        B, Hk, S, hd = c.max_batch, c.n_kv_heads, info["slots"], c.head_dim
+        n = B * Hk * S * hd
+
+        def view(off):
+            raw = self.state[off: off + n * es]
+            if es == 2:  # bf16 bits -> float32
+                return (raw.view(torch.int16).to(torch.int32) << 16).view(torch.float32)
+            return raw.view(torch.float32)
+        K = view(info["k_offset"]).view(B, Hk, S, hd)[: self.batch, :, :n_slots]
+        V = view(info["v_offset"]).view(B, Hk, S // 32, hd, 32).permute(0, 1, 2, 4, 3).reshape(B, Hk, S, hd)
+        return K.clone(), V[: self.batch, :, :n_slots].clone()
 
     def macro_step(self, forced=None, teacher=None):
         ham_macro_step(self.handle, forced, teacher, self.out_tokens, self.out_lens)

@@ -19,6 +19,10 @@ from synth.configs import BF16, STOP_FORCED, HamShape
 
 TOL = {0: 1e-4, BF16: 2e-2}
 
+# a small bf16 model of several tiles per GEMM dimension, FORCED stops
+SMALL16 = HamShape(n_layers=4, d_model=512, n_heads=8, n_kv_heads=2, head_dim=64, ffn_dim=1024, vocab=4096,
+                   micro_layers=2, max_group=4, stop_mode=STOP_FORCED, stop_id=1023, dtype=BF16)
+
 
 def config_for(shape: HamShape, batch: int, prompt: int, steps: int):
     from paper_2505_20438_amd import ham

@@ -90,6 +90,7 @@ def test_calls_on_null_handle(lib):
     assert lib.ham_macro_step(None, None, None, None, None) == ham.HAM_EINVAL
     assert lib.ham_prefill(None, 1, None, 1, None, None, None, None, None) == ham.HAM_EINVAL
     assert lib.ham_kv_stats(None, None) == ham.HAM_EINVAL
+    assert lib.ham_prefill_embeds(None, 1, None, None, 1, None, None, None, None, None) == ham.HAM_EINVAL
     assert lib.ham_steps_done(None) == -1
     lib.ham_destroy(None)
 
@@ -123,3 +124,24 @@ def test_op_attention_rejects_bad_shapes(lib):
     assert rc == ham.HAM_EINVAL
     rc = lib.ham_op_decode_attention(1, 4, 32, 8, 128, 4096, 256, 256, 256, 256, 256, 8, 256, 256, 16, None)
     assert rc == ham.HAM_ENOMEM
+
+
+def test_state_info_layout(lib):
+    cfg = config_for(TINY, 2, 64, 128)
+    total = ham.ham_state_bytes(cfg)
+    es = 4  # fp32 model
+    infos = [ham.ham_state_info(cfg, l) for l in range(TINY.n_layers)]
+    S = infos[0]["slots"]
+    assert S % 64 == 0 and S >= 64 + 128
+    per_layer = 2 * TINY.n_kv_heads * S * TINY.head_dim * es
+    spans = []
+    for i in infos:
+        assert i["slots"] == S and i["k_offset"] % 256 == 0 and i["v_offset"] % 256 == 0
+        spans += [(i["k_offset"], i["k_offset"] + per_layer), (i["v_offset"], i["v_offset"] + per_layer)]
+    spans.sort()
+    assert spans[-1][1] <= total
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))   # K and V of all layers are disjoint
+    with pytest.raises(ham.HamError):
+        ham.ham_state_info(cfg, TINY.n_layers)
+    with pytest.raises(ham.HamError):
+        ham.ham_state_info(cfg, -1)

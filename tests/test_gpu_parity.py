@@ -10,7 +10,7 @@ import pytest
 import synth
 from oracle import OracleHam
 from synth.configs import BF16, SHAPE_1B, STOP_FORCED, STOP_HEAD, STOP_TOKEN, TINY, WORKLOADS
-from tests.gpu_util import TOL, check_decision, config_for, oracle_groups_for, run_gpu
+from tests.gpu_util import SMALL16, TOL, check_decision, config_for, oracle_groups_for, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -91,8 +91,6 @@ def test_tiny_fp32_free_running_exact(torch_cuda, mode):
     assert sum(st["len_hist"]) == len(orc.groups)
 
 
-SMALL16 = dataclasses.replace(TINY, n_layers=4, d_model=512, n_heads=8, n_kv_heads=2, head_dim=64, ffn_dim=1024,
-                              vocab=4096, micro_layers=2, stop_mode=STOP_FORCED, dtype=BF16)
 
 
 def _teacher_forced(om, shp, prompts, budgets, steps, sched, seed, debug_steps):

@@ -68,12 +68,12 @@ struct SkinnyBatch {
 // fragment f of every operand: weight block (tile j, f) at wrow[j] + f*512 elements-of-16B
 template <typename T, int MT, int TN>
 __device__ __forceinline__ void skinny_load(SkinnyBatch<T, MT, TN>& b, const T* const* wrow, const T* const* xrow,
-                                            const bool* xok, int lo_off, int f) {
+                                            const bool* xok, int lo_off, int f, int stride) {
   constexpr int KB = Frag<T>::KB, EPL = Frag<T>::EPL, U = SkinnyBatch<T, MT, TN>::U;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) b.w[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * 64 * EPL);
+    for (int j = 0; j < TN; ++j) b.w[u][j] = ld16_stream(wrow[j] + (size_t)(f + u * stride) * 64 * EPL);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       // only lanes of live rows load (rows past M would fetch 1 KB per wave
@@ -81,8 +81,8 @@ __device__ __forceinline__ void skinny_load(SkinnyBatch<T, MT, TN>& b, const T* 
       b.xh[u][i] = zero16();
       b.xl[u][i] = zero16();
       if (xok[i]) {
-        b.xh[u][i] = ld16(xrow[i] + (size_t)(f + u) * KB);
-        if constexpr (Act<T>::SPLIT) b.xl[u][i] = ld16(xrow[i] + lo_off + (size_t)(f + u) * KB);
+        b.xh[u][i] = ld16(xrow[i] + (size_t)(f + u * stride) * KB);
+        if constexpr (Act<T>::SPLIT) b.xl[u][i] = ld16(xrow[i] + lo_off + (size_t)(f + u * stride) * KB);
       }
     }
   }
@@ -120,7 +120,9 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   const int n0 = ntile * 16 * TN;
   const int nfr = a.K / KB;
   const int c0 = (int)((long)split * nfr / nsplit), c1 = (int)((long)(split + 1) * nfr / nsplit);
-  const int f0 = c0 + w * (c1 - c0) / 4, f1 = c0 + (w + 1) * (c1 - c0) / 4;
+  // wave w takes fragments c0 + w + 4i of the k-range: at any moment the four
+  // waves read neighbouring 1 KB blocks of a tile (one contiguous window)
+  const int nk = c1 - c0, cnt = nk > w ? (nk - w + 3) / 4 : 0;
   const T* W = (const T*)a.W;
   const T* X = (const T*)a.X;
 
@@ -146,16 +148,17 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
 
   // software pipeline over batches of U fragments: the loads of batch i+1 are
   // in flight while batch i feeds the matrix cores
-  const int nb = (f1 - f0) / U;
+  const int nb = cnt / U;
   SkinnyBatch<T, MT, TN> cur, nxt;
-  if (nb > 0) skinny_load<T, MT, TN>(cur, wrow, xrow, xok, lo_off, f0);
+  if (nb > 0) skinny_load<T, MT, TN>(cur, wrow, xrow, xok, lo_off, c0 + w, 4);
   for (int it = 0; it < nb; ++it) {
     const bool more = it + 1 < nb;
-    if (more) skinny_load<T, MT, TN>(nxt, wrow, xrow, xok, lo_off, f0 + (it + 1) * U);
+    if (more) skinny_load<T, MT, TN>(nxt, wrow, xrow, xok, lo_off, c0 + w + 4 * (it + 1) * U, 4);
     skinny_mma<T, MT, TN>(acc, cur);
     if (more) cur = nxt;
   }
-  for (int f = f0 + nb * U; f < f1; ++f) {
+  for (int i = nb * U; i < cnt; ++i) {
+    const int f = c0 + w + 4 * i;
     u4 bw[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * 64 * EPL);
@@ -506,7 +509,10 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
   const int nfr = a.K / KB;
   const int c0 = (int)((long)split * nfr / nsplit), c1 = (int)((long)(split + 1) * nfr / nsplit);
   const int Kr = (c1 - c0) * KB;
-  const int f0 = c0 + w * (c1 - c0) / STG_NW, f1 = c0 + (w + 1) * (c1 - c0) / STG_NW;
+  // wave w takes fragments c0 + w + STG_NW*i of the k-range: at any moment the
+  // waves of a workgroup read neighbouring 1 KB blocks of a tile
+  const int nk = c1 - c0, cnt = nk > w ? (nk - w + STG_NW - 1) / STG_NW : 0;
+  const auto FR = [&](int i) { return c0 + w + STG_NW * i; };
   float* red = dsm;
   char* stg = reinterpret_cast<char*>(dsm + (STG_NW - 1) * TN * 4 * 64);
   float* aux = reinterpret_cast<float*>(stg + (size_t)a.M * 4 * Kr);
@@ -522,7 +528,7 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
   else stage_attn_load(a, pl, c0 * KB, Kr);
   __builtin_amdgcn_sched_barrier(0);
   constexpr int PF = 8 / TN;
-  const int npf = min(PF, f1 - f0);
+  const int npf = min(PF, cnt);
   u4 wp[PF][TN];
   {  // range-checked: blocks past this wave's k-range read zeros, fetch nothing
     const BufRsrc rw = buf_rsrc(W, (uint32_t)((size_t)a.N * a.K * sizeof(T)));
@@ -530,7 +536,7 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
     for (int u = 0; u < PF; ++u)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        wp[u][j] = buf_u4_stream(rw, u < npf ? (uint32_t)(((size_t)(n0 / 16 + j) * nfr + f0 + u) * 64 * EPL +
+        wp[u][j] = buf_u4_stream(rw, u < npf ? (uint32_t)(((size_t)(n0 / 16 + j) * nfr + FR(u)) * 64 * EPL +
                                                           (size_t)lane * EPL) * (uint32_t)sizeof(T)
                                              : BUF_OOB);
   }
@@ -538,14 +544,14 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
   if constexpr (XS == XS_NORM) stage_norm<T>(a, pl, stg, aux, c0 * KB, Kr, split, ntile == 0);
   else stage_attn<T>(a, pl, stg, aux, c0 * KB, Kr);
   __syncthreads();
-  const int fr0 = f0 + npf;
-  const int nb = (f1 - fr0) / U;
+  const int i0 = npf;
+  const int nb = (cnt - i0) / U;
   u4 wc[U][TN], wn[U][TN];
-  auto wload = [&](u4 (*dst)[TN], int f) {
+  auto wload = [&](u4 (*dst)[TN], int i) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int j = 0; j < TN; ++j) dst[u][j] = ld16_stream(wrow[j] + (size_t)(f + u) * 64 * EPL);
+      for (int j = 0; j < TN; ++j) dst[u][j] = ld16_stream(wrow[j] + (size_t)FR(i + u) * 64 * EPL);
   };
   const bool xrow = r16 < a.M;
   const char* xb = stg + (size_t)(xrow ? r16 : 0) * 4 * Kr + (size_t)g * EPL * sizeof(T);
@@ -561,20 +567,20 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
   for (int u = 0; u < PF; ++u)
     if (u < npf) {
       u4 h, l;
-      xfrag(f0 + u, h, l);
+      xfrag(FR(u), h, l);
 #pragma unroll
       for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, wp[u][j]);
     }
   // the rest in batches of U; issuing the first batch only once the prefetched
   // blocks have arrived measured faster than issuing it right after the prologue
-  if (nb > 0) wload(wc, fr0);
+  if (nb > 0) wload(wc, i0);
   for (int it = 0; it < nb; ++it) {
     const bool more = it + 1 < nb;
-    if (more) wload(wn, fr0 + (it + 1) * U);
+    if (more) wload(wn, i0 + (it + 1) * U);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       u4 h, l;
-      xfrag(fr0 + it * U + u, h, l);
+      xfrag(FR(i0 + it * U + u), h, l);
 #pragma unroll
       for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, wc[u][j]);
     }
@@ -585,7 +591,8 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
         for (int j = 0; j < TN; ++j) wc[u][j] = wn[u][j];
     }
   }
-  for (int f = fr0 + nb * U; f < f1; ++f) {
+  for (int i = i0 + nb * U; i < cnt; ++i) {
+    const int f = FR(i);
     u4 bw[TN], h, l;
 #pragma unroll
     for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * 64 * EPL);

@@ -216,6 +216,8 @@ def main() -> int:
                     help="first run one plain device-to-device copy of this size (HBM counter calibration)")
     ap.add_argument("--base", choices=("auto", "on", "off"), default="auto",
                     help="also time the same model decoding one token per forward (groups of one; auto: prompts <= 4096)")
+    ap.add_argument("--graph", choices=("on", "off"), default="on",
+                    help="replay each macro-step's launches from a HIP graph (on) or launch them on the stream")
     ap.add_argument("--head-sweep", default="",
                     help="comma-separated confidences: also time the model-driven stop head (HEAD mode) at each")
     args = ap.parse_args()
@@ -238,6 +240,7 @@ def main() -> int:
                           max_group=s.max_group, stop_mode=s.stop_mode, stop_id=s.stop_id, dtype=s.dtype,
                           max_batch=B, max_prompt=P, max_steps=w.max_new)
     rt = ham.HamRuntime(cfg, w.seed_weights, "cuda:0")
+    rt.set_graph(args.graph == "on")
     stream = rt.stream
     prompts = torch.from_numpy(synth.prompt_ids(w.seed_prompt, B, P, s.vocab)).to(dev)
     sched_np = synth.group_schedule(w.seed_sched, B, w.max_new + 1, s.max_group)
@@ -264,14 +267,17 @@ def main() -> int:
         e1.record(stream)
         if profile:
             ham.load_library().ham_profile(rt.handle, 1)
+        h0 = time.perf_counter()
         for st in range(1, n_steps + 1):
             rt.macro_step(sched[st])
+        host_enqueue.append(time.perf_counter() - h0)
         e2.record(stream)
         if profile:
             ham.load_library().ham_profile(rt.handle, 0)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1), e1.elapsed_time(e2)
 
+    host_enqueue = []
     for _ in range(args.warmup):
         one_run()
     torch.cuda.synchronize()
@@ -329,6 +335,8 @@ def main() -> int:
         "algorithmic_bytes_per_run": alg_bytes,
         "prefill_ms": float(np.mean(prefill_ms)),
         "us_per_macro_step": 1000.0 * dec_ms / n_steps,
+        "host_enqueue_us_per_macro_step": 1e6 * float(np.median(host_enqueue[args.warmup:args.warmup + args.steps])) / n_steps,
+        "graph": args.graph == "on",
         "wall_s_timed": wall,
         "roofline": roofline,
         "kernels": kernels,

@@ -177,6 +177,15 @@ int ham_set_debug(ham_model* m, void* d_buf, size_t bytes);
 /* Number of macro-steps run since the last prefill, or -1. */
 int ham_steps_done(const ham_model* m);
 
+/* Diagnostics: whether ham_macro_step replays its launches from a HIP graph
+ * (enable = 1, the default) or launches each kernel on the stream (0).  The
+ * graph holds every launch after the step's first kernel, captured once and
+ * replayed while the batch, prompt length, output pointers, debug buffer and
+ * teacher forcing stay the same; the kernels and their arguments are
+ * identical either way (a dependent launch costs about 0.6 us less from a
+ * graph).  Timing (ham_profile) always launches on the stream. */
+int ham_set_graph(ham_model* m, int enable);
+
 /* Where one generated tensor lives in the weights buffer, by the tensor id of
  * the initialiser (0 E, 1 P, 2..6 A_q A_k A_v A_o A_lin, 7 LM head, 8 stop
  * head, 16 + 8j + t for layer j (base layers first, then micro layers),

@@ -209,6 +209,31 @@ struct ham_model {
   int prof_kind = -1;
   double prof_bytes = 0;
   hipEvent_t prof_a = nullptr;
+  // The launches of a macro-step after k_macro_begin, captured once as a HIP
+  // graph and replayed (a dependent launch costs ~0.6 us less from a graph).
+  // Everything they depend on is fixed until the key changes.
+  struct GraphKey {
+    int batch = -1, prompt_len = -1, has_teacher = -1;
+    const void* out_tokens = nullptr;
+    const void* out_lens = nullptr;
+    const void* dbg = nullptr;
+    bool operator==(const GraphKey& o) const {
+      return batch == o.batch && prompt_len == o.prompt_len && has_teacher == o.has_teacher &&
+             out_tokens == o.out_tokens && out_lens == o.out_lens && dbg == o.dbg;
+    }
+  };
+  bool use_graph = true;
+  hipStream_t cap_stream = nullptr;  // private stream the graph is captured on (launched on s)
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  GraphKey gkey;
+  void drop_graph() {
+    if (gexec) hipGraphExecDestroy(gexec);
+    if (graph) hipGraphDestroy(graph);
+    gexec = nullptr;
+    graph = nullptr;
+    gkey = GraphKey{};
+  }
   // the next kernel launched is timed by events attached to its dispatch
   void pbegin(int kind, double bytes) {
     if (!prof_on || kind < 0) return;
@@ -226,6 +251,8 @@ struct ham_model {
     prof_a = nullptr;
   }
   ~ham_model() {
+    drop_graph();
+    if (cap_stream) hipStreamDestroy(cap_stream);
     for (hipEvent_t e : pool) hipEventDestroy(e);
   }
   // typed views
@@ -795,30 +822,20 @@ int ham_prefill_embeds(ham_model* m, int32_t batch, const float* d_embeds, const
                         d_out_tokens, d_out_lens);
 }
 
-int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens,
-                   int32_t* d_out_lens) {
-  if (!m) return fail(HAM_EINVAL, "null model");
-  if (m->steps_done < 0) return fail(HAM_ESTATE, "ham_macro_step before ham_prefill");
-  if (!d_out_tokens || !d_out_lens) return fail(HAM_EINVAL, "null output");
+}  // extern "C"
+
+namespace {
+
+// Everything of a macro-step after k_macro_begin: the embedder, the base
+// forward writing one KV slot per running sequence, the decisions and the
+// micro loop.  Launch arguments depend only on the batch, the prompt length,
+// the output pointers, the debug buffer and teacher forcing.
+int macro_step_body(ham_model* m, int32_t* d_out_tokens, int32_t* d_out_lens) {
   const Layout& y = m->y;
-  if (m->steps_done >= y.steps) return fail(HAM_ECAP, "max_steps (%d) reached", y.steps);
-  if (m->prompt_len + m->steps_done + 1 > y.S)
-    return fail(HAM_ECAP, "KV slot capacity (%d) reached", y.S);
-  if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
-  if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
   const int B = m->batch;
-  m->has_teacher = d_teacher != nullptr;
   float* x = m->WS<float>(y.x);
-  MacroArgs ma{};
-  ma.st = m->sp; ma.B = B; ma.d = y.d; ma.G = y.G; ma.E = m->W<char>(y.E); ma.P = m->W<char>(y.Pe); ma.x = x;
-  ma.ldx = y.d; ma.emb_in = m->WS<char>(y.emb_in); ma.forced_in = d_forced_lens; ma.teacher_in = d_teacher;
-  ma.out_tokens = d_out_tokens; ma.out_lens = d_out_lens;
-  ma.cos_t = m->W<float>(y.cos_t); ma.sin_t = m->W<float>(y.sin_t); ma.max_pos = y.max_pos; ma.hd = y.hd;
-  ma.rope_cs = m->WS<float>(y.rope_cs);
-  launch_macro_begin(dt, ma, s);
-
   // compositional embedder (Sec. 3.2), skipped on device unless some group has > 1 token
   GemmArgs ga{};
   ga.part = m->WS<float>(y.part); ga.gate = m->sp.fused; ga.gate_n = B;
@@ -850,10 +867,12 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   RowMap rm{};
   rm.mode = ROWS_DECODE; rm.st = m->sp;
   const long long sb = (long long)y.Hk * y.S * y.hd, sh = (long long)y.S * y.hd;
-  const int kv_max = m->prompt_len + m->steps_done + 1;  // every sequence holds at most this many slots now
-  const int nsplit = attn_step_splits(dt, B, y.Hk, y.hd, kv_max - 1);
-  m->kv_visible = B * kv_max;
-  const StepAttn bstep{m->WS<float>(y.rope_cs), m->WS<float>(y.rope_cs) + y.hd / 2, y.hd, kv_max - 1};
+  // the attention launch is sized for the most slots any step of this generation
+  // can hold, so every macro-step launches the same kernels with the same
+  // arguments (graph replay); each row attends over its own device-side length
+  const int kv_cap = std::min(m->prompt_len + y.steps - 1, y.S - 1);
+  const int nsplit = attn_step_splits(dt, B, y.Hk, y.hd, kv_cap);
+  const StepAttn bstep{m->WS<float>(y.rope_cs), m->WS<float>(y.rope_cs) + y.hd / 2, y.hd, kv_cap};
   float* ctx = m->WS<float>(y.ctx);
   Pending pend;
   float* ctx_prev = nullptr;  // context slot of the previous layer's output, captured by the next norm
@@ -868,6 +887,78 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   int rc = decode_tail(m, pend, ctx_prev, x, d_out_tokens, d_out_lens);
   if (rc) return rc;
   HIP_TRY(hipGetLastError());
+  return HAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_teacher, int32_t* d_out_tokens,
+                   int32_t* d_out_lens) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  if (m->steps_done < 0) return fail(HAM_ESTATE, "ham_macro_step before ham_prefill");
+  if (!d_out_tokens || !d_out_lens) return fail(HAM_EINVAL, "null output");
+  const Layout& y = m->y;
+  if (m->steps_done >= y.steps) return fail(HAM_ECAP, "max_steps (%d) reached", y.steps);
+  if (m->prompt_len + m->steps_done + 1 > y.S)
+    return fail(HAM_ECAP, "KV slot capacity (%d) reached", y.S);
+  if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
+  if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
+  const int dt = dtype_of(m);
+  hipStream_t s = m->s;
+  const int B = m->batch;
+  m->has_teacher = d_teacher != nullptr;
+  float* x = m->WS<float>(y.x);
+  MacroArgs ma{};
+  ma.st = m->sp; ma.B = B; ma.d = y.d; ma.G = y.G; ma.E = m->W<char>(y.E); ma.P = m->W<char>(y.Pe); ma.x = x;
+  ma.ldx = y.d; ma.emb_in = m->WS<char>(y.emb_in); ma.forced_in = d_forced_lens; ma.teacher_in = d_teacher;
+  ma.out_tokens = d_out_tokens; ma.out_lens = d_out_lens;
+  ma.cos_t = m->W<float>(y.cos_t); ma.sin_t = m->W<float>(y.sin_t); ma.max_pos = y.max_pos; ma.hd = y.hd;
+  ma.rope_cs = m->WS<float>(y.rope_cs);
+  launch_macro_begin(dt, ma, s);
+  m->kv_visible = B * (m->prompt_len + m->steps_done + 1);  // slots attended this step (profiling bytes)
+
+  if (m->use_graph && !m->prof_on) {
+    const ham_model::GraphKey key{B, m->prompt_len, m->has_teacher, d_out_tokens, d_out_lens, m->dbg};
+    if (!(m->gexec && m->gkey == key)) {
+      m->drop_graph();
+      hipGraph_t g = nullptr;
+      // captured on a private stream (the caller's may be the legacy default
+      // stream, which cannot be captured), launched on the caller's stream
+      if (!m->cap_stream && hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking) != hipSuccess)
+        m->cap_stream = nullptr;
+      if (m->cap_stream && hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal) == hipSuccess) {
+        m->s = m->cap_stream;
+        const int rc = macro_step_body(m, d_out_tokens, d_out_lens);
+        m->s = s;
+        const hipError_t ec = hipStreamEndCapture(m->cap_stream, &g);
+        if (rc) {
+          if (g) hipGraphDestroy(g);
+          return rc;
+        }
+        if (ec == hipSuccess && g && hipGraphInstantiate(&m->gexec, g, nullptr, nullptr, 0) == hipSuccess) {
+          m->graph = g;
+          m->gkey = key;
+        } else {
+          if (g) hipGraphDestroy(g);
+          m->gexec = nullptr;
+          m->use_graph = false;  // capture unavailable: launch on the stream from now on
+          (void)hipGetLastError();
+        }
+      } else {
+        m->use_graph = false;
+        (void)hipGetLastError();
+      }
+    }
+    if (m->gexec) {
+      HIP_TRY(hipGraphLaunch(m->gexec, s));
+      m->steps_done += 1;
+      return HAM_OK;
+    }
+  }
+  const int rc = macro_step_body(m, d_out_tokens, d_out_lens);
+  if (rc) return rc;
   m->steps_done += 1;
   return HAM_OK;
 }
@@ -907,6 +998,13 @@ int ham_set_debug(ham_model* m, void* d_buf, size_t bytes) {
 }
 
 int ham_steps_done(const ham_model* m) { return m ? m->steps_done : -1; }
+
+int ham_set_graph(ham_model* m, int enable) {
+  if (!m) return fail(HAM_EINVAL, "null model");
+  m->drop_graph();
+  m->use_graph = enable != 0;
+  return HAM_OK;
+}
 
 int ham_profile(ham_model* m, int enable) {
   if (!m) return fail(HAM_EINVAL, "null model");

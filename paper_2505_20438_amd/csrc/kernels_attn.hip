@@ -462,33 +462,65 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
 #pragma unroll
   for (int i = 0; i < NB; ++i)
     if (b0 + i < b1) attn_block<T, HD>(blk[i], (b0 + i) * KB, limit, limit, qf, ql, scale, mrun, lrun, o);
-  attn_blocks<T, HD>(Kb, Vb, a.S, 0, b0 + NB, b1, limit, limit, qf, ql, scale, mrun, lrun, o);
+  // kv_cap bounds every row of the launch; this row's own length ends the loop
+  attn_blocks<T, HD>(Kb, Vb, a.S, 0, b0 + NB, min(b1, (limit + KB - 1) / KB), limit, limit, qf, ql, scale, mrun,
+                     lrun, o);
   attn_publish<T, HD>(sh, grp, mrun, lrun, o);
   __syncthreads();
   attn_merge_store<T, HD>(sh, extra, grp, r, a.R, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part_out);
 }
 
-// Log-sum-exp combine of the splits of one (row, head), in split order.
+// Log-sum-exp combine of the splits of one (row, head) (nsplit <= 64): lane s
+// of wave 0 holds split s and forms its weight exp(m_s - M) / L with wave
+// reductions; then thread t sums the weighted outputs of element t % hd over
+// splits t / hd, t / hd + G, ... (G = 256 / hd, all loads of a thread in flight
+// together) and the G partial sums are added in order.
+constexpr int COMBINE_THREADS = 256;
 template <typename T>
-__global__ __launch_bounds__(64) void k_attn_combine(AttnArgs a) {
+__global__ __launch_bounds__(COMBINE_THREADS) void k_attn_combine(AttnArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
-  const int r = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-  const int grp = a.H / a.Hkv, kvh = h / grp, j = h % grp, HD = a.hd;
-  const float* ml = a.part + (size_t)a.R * a.Hkv * a.nsplit * grp * HD;
-  float M = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, ml[2 * attn_rec(r, kvh, s, j, a.Hkv, a.nsplit, grp)]);
-  for (int d = lane; d < HD; d += 64) {
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-      for (int s = 0; s < a.nsplit; ++s) {
-        const size_t q = attn_rec(r, kvh, s, j, a.Hkv, a.nsplit, grp);
-        const float ms = ml[2 * q];
-        const float wgt = ms == -INFINITY ? 0.f : __expf(ms - M);
-        L += wgt * ml[2 * q + 1];
-        O += wgt * a.part[q * HD + d];
+  __shared__ float wts[64];
+  __shared__ float acc[COMBINE_THREADS];
+  const int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+  const int grp = a.H / a.Hkv, kvh = h / grp, j = h % grp, HD = a.hd, ns = a.nsplit;
+  const float* ml = a.part + (size_t)a.R * a.Hkv * ns * grp * HD;
+  if (tid < 64) {
+    float ms = -INFINITY, ls = 0.f;
+    if (lane < ns) {
+      const size_t q = attn_rec(r, kvh, lane, j, a.Hkv, ns, grp);
+      ms = ml[2 * q];
+      ls = ml[2 * q + 1];
+    }
+    const float M = wave_max(ms);
+    const float e = (ms == -INFINITY) ? 0.f : __expf(ms - M);
+    const float L = wave_sum(e * ls);
+    if (lane < ns) wts[lane] = L > 0.f ? e / L : 0.f;
+  }
+  __syncthreads();
+  const int G = COMBINE_THREADS / HD, d = tid % HD, sg = tid / HD;
+  float o = 0.f;
+  if (sg < G) {
+    constexpr int UN = 8;
+    for (int s0 = sg; s0 < ns; s0 += G * UN) {
+      float v[UN];
+#pragma unroll
+      for (int u = 0; u < UN; ++u) {
+        const int sp = s0 + u * G;
+        v[u] = sp < ns ? a.part[attn_rec(r, kvh, sp, j, a.Hkv, ns, grp) * HD + d] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < UN; ++u) {
+        const int sp = s0 + u * G;
+        if (sp < ns) o += wts[sp] * v[u];
       }
     }
-    Act<T>::put(a.o, r, a.ldo, h * HD + d, L > 0.f ? O / L : 0.f);
+  }
+  acc[tid] = o;
+  __syncthreads();
+  if (tid < HD) {
+    float x = acc[tid];
+    for (int q = 1; q < G; ++q) x += acc[q * HD + tid];
+    Act<T>::put(a.o, r, a.ldo, h * HD + tid, x);
   }
 }
 
@@ -541,7 +573,7 @@ static int decode_t(const AttnArgs& a, Stream s) {
   if (a.hd == 64) launch_k((k_attn_decode<T, 64>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else if (a.hd == 128) launch_k((k_attn_decode<T, 128>), grid, dim3(64 * ATTN_NW), 0, s, a);
   else return -1;
-  if (a.nsplit > 1) launch_k((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, a);
+  if (a.nsplit > 1) launch_k((k_attn_combine<T>), dim3(a.R, a.H), dim3(COMBINE_THREADS), 0, s, a);
   return 0;
 }
 template <typename T>
@@ -563,7 +595,7 @@ static int step_t(const AttnStepArgs& a, Stream s) {
     AttnArgs c{};
     c.H = a.H; c.Hkv = a.Hkv; c.hd = a.hd; c.R = a.R; c.nsplit = a.nsplit; c.o = a.o; c.ldo = a.ldo;
     c.part = a.part_out;
-    launch_k((k_attn_combine<T>), dim3(a.R, a.H), dim3(64), 0, s, c);
+    launch_k((k_attn_combine<T>), dim3(a.R, a.H), dim3(COMBINE_THREADS), 0, s, c);
   }
   return 0;
 }
@@ -572,7 +604,8 @@ int attn_step_max_qkv_split() { return ATTN_STEP_MAXS; }
 
 int launch_attn_step(int dtype, const AttnStepArgs& a, Stream s) {
   if (a.R <= 0) return 0;
-  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 4 || a.S % 64 != 0 || a.kv_cap < 0 || a.kv_cap > a.S || a.nsplit < 1)
+  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 4 || a.S % 64 != 0 || a.kv_cap < 0 || a.kv_cap > a.S || a.nsplit < 1 ||
+      a.nsplit > 64)  // the split combine holds one split per lane
     return -1;
   if (a.part && (a.nsplit_qkv < 1 || a.nsplit_qkv > ATTN_STEP_MAXS)) return -1;
   if (a.rm.mode != ROWS_DECODE && a.rm.mode != ROWS_MICROK) return -1;
@@ -580,7 +613,7 @@ int launch_attn_step(int dtype, const AttnStepArgs& a, Stream s) {
 }
 
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s) {
-  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 4 || a.S % 64 != 0) return -1;
+  if (a.H % a.Hkv != 0 || a.H / a.Hkv > 4 || a.S % 64 != 0 || a.nsplit < 1 || a.nsplit > 64) return -1;
   return dtype == 1 ? decode_t<bf16>(a, s) : decode_t<float>(a, s);
 }
 int launch_attn_prefill(int dtype, const AttnArgs& a, Stream s) {

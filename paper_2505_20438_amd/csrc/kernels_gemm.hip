@@ -945,6 +945,8 @@ static int gemm_staged(const GemmArgs& a0, int max_split, int tag, Stream s, int
     if (a.xs.part && (a.xs.nsplit < 1 || a.xs.nsplit > STG_SMAX)) return GEMM_NO_STAGE;
     if (nsplit > 1 && !a.xs.ss_out) return GEMM_NO_STAGE;
   } else {
+    // every workgroup reads the attention records of its k-range: only while
+    // there are few of them (a thread combines at most STG_AMAX splits)
     const int nch = a.M * Kr / 4, ans = a.xs.ans;
     if (nch > STG_THREADS || ans > 64) return GEMM_NO_STAGE;
     const int SG = std::max(1, std::min(STG_THREADS / nch, ans));

@@ -21,7 +21,7 @@ HAM_PROF_KINDS = 9
 
 EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
             "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
-            "ham_tensor_info", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
+            "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
             "ham_op_attention_workspace_bytes", "ham_op_decode_attention")
 
 
@@ -81,6 +81,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_steps_done.argtypes = [P]
     lib.ham_tensor_info.argtypes = [cfgp, I32, ctypes.POINTER(SZ)] + [ctypes.POINTER(I32)] * 6
     lib.ham_profile.argtypes = [P, I32]
+    lib.ham_set_graph.argtypes = [P, I32]
     lib.ham_profile_read.argtypes = [P, ctypes.POINTER(HamProfT), I32]
     lib.ham_op_attention_workspace_bytes.argtypes = [I32, I32, I32, I32]
     lib.ham_op_attention_workspace_bytes.restype = SZ
@@ -90,7 +91,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_destroy.argtypes = [P]
     lib.ham_destroy.restype = None
     for n in ("ham_init_weights", "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug",
-              "ham_steps_done", "ham_tensor_info", "ham_profile", "ham_profile_read"):
+              "ham_steps_done", "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read"):
         getattr(lib, n).restype = I32
     _lib = lib
     return lib
@@ -262,6 +263,9 @@ class HamRuntime:
 
     def macro_step(self, forced=None, teacher=None):
         ham_macro_step(self.handle, forced, teacher, self.out_tokens, self.out_lens)
+
+    def set_graph(self, enable: bool) -> None:
+        _check(load_library().ham_set_graph(self.handle, 1 if enable else 0))
 
     def kv_stats(self):
         return ham_kv_stats(self.handle, self.batch)

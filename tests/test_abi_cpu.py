@@ -91,6 +91,7 @@ def test_calls_on_null_handle(lib):
     assert lib.ham_prefill(None, 1, None, 1, None, None, None, None, None) == ham.HAM_EINVAL
     assert lib.ham_kv_stats(None, None) == ham.HAM_EINVAL
     assert lib.ham_prefill_embeds(None, 1, None, None, 1, None, None, None, None, None) == ham.HAM_EINVAL
+    assert lib.ham_set_graph(None, 1) == ham.HAM_EINVAL
     assert lib.ham_steps_done(None) == -1
     lib.ham_destroy(None)
 

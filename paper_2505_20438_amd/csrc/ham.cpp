@@ -299,7 +299,7 @@ int gemm_p(ham_model* m, int epi, const GemmArgs& a, int max_split, int kind, in
 
 // RMSNorm of R rows of x (row r reads x row r*stride + off) into the operand buffer,
 // after adding a pending split-K result to those rows and copying them to ctx
-void norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* g, Pending& pend, float* ctx,
+int norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* g, Pending& pend, float* ctx,
                int ldctx, float* hid, const int* gate, int gate_n) {
   const Layout& y = m->y;
   NormArgs na{};
@@ -307,8 +307,8 @@ void norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* 
   na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d; na.hid = hid; na.ldh = y.d;
   na.part = pend.part; na.nsplit = pend.nsplit; na.pM = pend.M; na.ctx = ctx; na.ldctx = ldctx;
   na.gate = gate; na.gate_n = gate_n;
-  launch_rmsnorm(dtype_of(m), na, m->s);
   pend = Pending{};
+  return launch_rmsnorm(dtype_of(m), na, m->s) ? fail(HAM_EINVAL, "rmsnorm shape") : HAM_OK;
 }
 
 // The rest of a layer after attention: o-projection into the residual, second
@@ -325,7 +325,7 @@ int layer_tail(ham_model* m, int j, int R, float* x, int split, const int* gate,
   if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_O), &ns)) return fail(HAM_EINVAL, "o-proj gemm shape");
   if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
 
-  norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n);
+  if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n)) return HAM_EINVAL;
 
   ga.W = m->W<char>(y.Wgu[j]); ga.N = 2 * y.F; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
   ga.out = m->WS<char>(y.act); ga.ldo = y.F;
@@ -395,7 +395,7 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   const int qkv_split = std::min(split, attn_step_max_qkv_split());
   const bool q_staged = gemm_stage_fits(dt, EPI_F32, ga, qkv_split);
   if (!q_staged) {
-    norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
+    if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n)) return HAM_EINVAL;
     ga.xsrc = XS_ACT; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
   }
   if (gemm_p(m, EPI_F32, ga, qkv_split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
@@ -444,7 +444,7 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   gu.xs.g = m->W<float>(y.g2[j]); gu.xs.eps = eps; gu.xs.x_out = other(x);
   const bool u_staged = gemm_stage_fits(dt, EPI_SWIGLU, gu, 1);
   if (!u_staged) {
-    norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n);
+    if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n)) return HAM_EINVAL;
     gu.xsrc = XS_ACT; gu.X = m->WS<char>(y.xn); gu.ldx = y.d;
   }
   if (gemm_p(m, EPI_SWIGLU, gu, 1, gk(HAM_PROF_GU), &ns)) return fail(HAM_EINVAL, "gate/up gemm shape");
@@ -482,7 +482,7 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool pref
                           kv_visible, *step, base);
   const int split = prefill ? 1 : MAX_GEMM_SPLIT;
   int ns = 1;
-  norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n);
+  if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n)) return HAM_EINVAL;
 
   GemmArgs ga{};
   ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n;
@@ -517,7 +517,7 @@ int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, con
   const Layout& y = m->y;
   const int B = m->batch;
   float* hid = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + ((size_t)k * y.B) * y.d : nullptr;
-  norm_rows(m, x, B, row_stride, row_off, g, pend, ctx_last, y.C * y.d, hid, m->sp.active, B);
+  if (norm_rows(m, x, B, row_stride, row_off, g, pend, ctx_last, y.C * y.d, hid, m->sp.active, B)) return HAM_EINVAL;
 
   GemmArgs ga{};
   ga.W = m->W<char>(y.Wlm); ga.N = y.Vpad; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = B;
@@ -853,14 +853,14 @@ int macro_step_body(ham_model* m, int32_t* d_out_tokens, int32_t* d_out_lens) {
   if (gemm_p(m, EPI_OP, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
   if (ns > 1) {
     ga.nsplit = ns;
-    launch_split_reduce(dt, EPI_OP, ga, s);
+    if (launch_split_reduce(dt, EPI_OP, ga, s)) return fail(HAM_EINVAL, "split reduce shape");
   }
   ga.W = m->W<char>(y.Alin); ga.N = y.d; ga.K = y.d; ga.X = m->WS<char>(y.emb_y); ga.ldx = y.d;
   ga.out = x; ga.ldo = y.d; ga.rowmask = m->sp.fused;
   if (gemm_p(m, EPI_XMASK, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
   if (ns > 1) {
     ga.nsplit = ns;
-    launch_split_reduce(dt, EPI_XMASK, ga, s);
+    if (launch_split_reduce(dt, EPI_XMASK, ga, s)) return fail(HAM_EINVAL, "split reduce shape");
   }
 
   // base forward: one new KV slot per running sequence

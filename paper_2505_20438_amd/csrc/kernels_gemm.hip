@@ -761,34 +761,53 @@ __global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int nti
 
 // Sum the split-K partials of a GEMM in split order and apply its epilogue.
 // SwiGLU: output feature f pairs gate column 16*(f/8) + f%8 with the up column 8 after it.
+// Grid (output columns / 256, rows): one output per thread, its partial loads
+// (nsplit <= SPLIT_RED_MAX) all in flight before they are added in split order.
+constexpr int SPLIT_RED_MAX = 16;
 template <typename T, int EPI>
 __global__ __launch_bounds__(256) void k_split_reduce(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
-  const int m = blockIdx.x;
+  const int m = blockIdx.y;
   const float* pm = a.part + (size_t)m * a.N;
   const size_t ss = (size_t)a.M * a.N;
+  const int ns = a.nsplit;
   if constexpr (EPI == EPI_SWIGLU) {
-    for (int f = threadIdx.x; f < a.N / 2; f += 256) {
-      const int ng = (f / 8) * 16 + f % 8;
-      float gv = 0.f, uv = 0.f;
-      for (int s = 0; s < a.nsplit; ++s) {
-        gv += pm[s * ss + ng];
-        uv += pm[s * ss + ng + 8];
+    const int f = blockIdx.x * 256 + threadIdx.x;
+    if (f >= a.N / 2) return;
+    const int ng = (f / 8) * 16 + f % 8;
+    float g[SPLIT_RED_MAX], u[SPLIT_RED_MAX];
+#pragma unroll
+    for (int s = 0; s < SPLIT_RED_MAX; ++s)
+      if (s < ns) {
+        g[s] = pm[s * ss + ng];
+        u[s] = pm[s * ss + ng + 8];
       }
-      Act<T>::put(a.out, m, a.ldo, f, gv / (1.0f + expf(-gv)) * uv);
-    }
+    float gv = 0.f, uv = 0.f;
+#pragma unroll
+    for (int s = 0; s < SPLIT_RED_MAX; ++s)
+      if (s < ns) {
+        gv += g[s];
+        uv += u[s];
+      }
+    Act<T>::put(a.out, m, a.ldo, f, gv / (1.0f + expf(-gv)) * uv);
     return;
   }
-  for (int n = threadIdx.x; n < a.N; n += 256) {
-    float v = 0.f;
-    for (int s = 0; s < a.nsplit; ++s) v += pm[s * ss + n];
-    if constexpr (EPI == EPI_OP) {
-      Act<T>::put(a.out, m, a.ldo, n, v);
-    } else if constexpr (EPI == EPI_XMASK) {
-      if (a.rowmask[m]) ((float*)a.out)[(size_t)m * a.ldo + n] = v;
-    } else {
-      ((float*)a.out)[(size_t)m * a.ldo + n] = v;
-    }
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  if (n >= a.N) return;
+  float p[SPLIT_RED_MAX];
+#pragma unroll
+  for (int s = 0; s < SPLIT_RED_MAX; ++s)
+    if (s < ns) p[s] = pm[s * ss + n];
+  float v = 0.f;
+#pragma unroll
+  for (int s = 0; s < SPLIT_RED_MAX; ++s)
+    if (s < ns) v += p[s];
+  if constexpr (EPI == EPI_OP) {
+    Act<T>::put(a.out, m, a.ldo, n, v);
+  } else if constexpr (EPI == EPI_XMASK) {
+    if (a.rowmask[m]) ((float*)a.out)[(size_t)m * a.ldo + n] = v;
+  } else {
+    ((float*)a.out)[(size_t)m * a.ldo + n] = v;
   }
 }
 
@@ -1000,7 +1019,8 @@ static int gemm_wide(GemmArgs a, int max_split, int tag, Stream s, int* nsplit_o
       else if (mt <= 10) HAM_WIDE(10, 1); else HAM_WIDE(16, 1);
     }
 #undef HAM_WIDE
-    if (EPI == EPI_SWIGLU && nsplit > 1) launch_k((k_split_reduce<T, EPI_SWIGLU>), dim3(a.M), dim3(256), 0, s, a);
+    if (EPI == EPI_SWIGLU && nsplit > 1)
+      launch_k((k_split_reduce<T, EPI_SWIGLU>), dim3((a.N / 2 + 255) / 256, a.M), dim3(256), 0, s, a);
     return 0;
   }
 
@@ -1081,7 +1101,8 @@ int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s) {
 }
 
 int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s) {
-  dim3 grid(a.M);
+  if (a.nsplit < 1 || a.nsplit > SPLIT_RED_MAX) return -1;
+  dim3 grid((a.N + 255) / 256, a.M);
 #define HAM_RED(EP)                                                                                     \
   do {                                                                                                  \
     if (dtype == 1) launch_k((k_split_reduce<bf16, EP>), grid, dim3(256), 0, s, a);           \

@@ -18,7 +18,8 @@ namespace ham {
 // 1024-thread block per row: every thread owns d/1024 columns and issues all of
 // its partial loads before summing them.
 constexpr int NORM_THREADS = 1024;
-constexpr int NORM_MAXV = 8;  // d <= 8192
+constexpr int NORM_MAXV = 8;   // d <= 8192
+constexpr int NORM_MAXS = 16;  // pending split-K partials
 
 template <typename T>
 __global__ __launch_bounds__(NORM_THREADS) void k_rmsnorm(NormArgs a) {
@@ -36,20 +37,21 @@ __global__ __launch_bounds__(NORM_THREADS) void k_rmsnorm(NormArgs a) {
     if (i < a.d) v[e] = x[i];
   }
   if (a.part) {
+    // per element, all partial loads in flight before they are added in split order
     const size_t sstride = (size_t)a.pM * a.ldx;
     const float* pp = a.part + (size_t)xr * a.ldx;
+    const int ns = a.nsplit;
 #pragma unroll
     for (int e = 0; e < NORM_MAXV; ++e) {
       const int i = threadIdx.x + e * NORM_THREADS;
       if (i < a.d) {
-        float p[4] = {0.f, 0.f, 0.f, 0.f};
-        int s = 0;
-        for (; s + 4 <= a.nsplit; s += 4) {
+        float p[NORM_MAXS];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) p[q] += pp[(size_t)(s + q) * sstride + i];
-        }
-        for (; s < a.nsplit; ++s) p[0] += pp[(size_t)s * sstride + i];
-        v[e] += ((p[0] + p[1]) + (p[2] + p[3]));
+        for (int q = 0; q < NORM_MAXS; ++q)
+          if (q < ns) p[q] = pp[(size_t)q * sstride + i];
+#pragma unroll
+        for (int q = 0; q < NORM_MAXS; ++q)
+          if (q < ns) v[e] += p[q];
         x[i] = v[e];
       }
     }
@@ -82,7 +84,7 @@ __global__ __launch_bounds__(NORM_THREADS) void k_rmsnorm(NormArgs a) {
 
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
   if (a.R <= 0) return 0;
-  if (a.d > NORM_THREADS * NORM_MAXV) return -1;
+  if (a.d > NORM_THREADS * NORM_MAXV || (a.part && (a.nsplit < 1 || a.nsplit > NORM_MAXS))) return -1;
   if (dtype == 1) launch_k((k_rmsnorm<bf16>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
   else launch_k((k_rmsnorm<float>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
   return 0;

@@ -75,7 +75,7 @@ def group_lengths(sched: np.ndarray, budget: int) -> list:
     return out
 
 
-def algorithmic_bytes(w: Workload, lens: list, max_steps: int = 0) -> float:
+def algorithmic_bytes(w: Workload, lens: list, max_steps: int = 0, token_variant: bool = False) -> float:
     """Bytes the decode loop must move (closed form over the realised schedule).
 
     Per macro-step s (consuming group s-1, emitting group s), while any sequence
@@ -83,6 +83,8 @@ def algorithmic_bytes(w: Workload, lens: list, max_steps: int = 0) -> float:
     consumed group has more than one token; for every micro step some sequence
     still needs, the micro-decoder weights and the LM head again; per running
     sequence the K and V of every visible slot, plus the new slot written.
+    With ``token_variant`` a group of n < max_group tokens (not cut by the
+    budget) takes one more micro step: the decision taken as the reserved id.
     """
     s = w.shape
     es = 2 if s.dtype == BF16 else 4
@@ -103,7 +105,11 @@ def algorithmic_bytes(w: Workload, lens: list, max_steps: int = 0) -> float:
         total += W_base + W_lm
         if any(lens[b][st - 1] > 1 for b in run):
             total += W_emb
-        micro = max(lens[b][st] for b in run) - 1
+        def steps_of(b):
+            n = lens[b][st]
+            cut = st == len(lens[b]) - 1 and sum(lens[b]) == w.max_new  # the budget ends this group
+            return n if (token_variant and n < s.max_group and not cut) else n - 1
+        micro = max(steps_of(b) for b in run)
         total += micro * (W_micro + W_lm)
         for b in run:
             kv_len = w.prompt_len + st
@@ -171,6 +177,36 @@ def base_comparator(w: Workload, prompts, warmup: int, steps: int) -> dict:
             "what": "same weights and kernels, max group 1: plain one-token-per-forward decoding"}
 
 
+def token_cost_run(w: Workload, prompts, sched, lens, n_steps: int, warmup: int, steps: int) -> dict:
+    """The same forced schedule with the reserved-token variant's control flow
+    (Sec. 4.4): a group shorter than the cap ends on one more micro step, whose
+    decision is discarded.  Emits the same tokens; measures that step's cost."""
+    import torch
+    from paper_2505_20438_amd import ham
+    rt = ham.HamRuntime(_config(w, stop_mode=ham.HAM_STOP_FORCED_TOKEN), w.seed_weights, "cuda:0")
+    B = w.batch
+    times = []
+    for i in range(warmup + steps):
+        rt.prefill(prompts, [w.max_new] * B, sched[0])
+        e1, e2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e1.record(rt.stream)
+        for st in range(1, n_steps + 1):
+            rt.macro_step(sched[st])
+        e2.record(rt.stream)
+        torch.cuda.synchronize()
+        if i >= warmup:
+            times.append(e1.elapsed_time(e2))
+    stats = rt.kv_stats()
+    assert all(st["tokens"] == w.max_new and st["device_error"] == 0 for st in stats), stats
+    ms = float(np.median(times))
+    nbytes = algorithmic_bytes(w, lens, n_steps, token_variant=True)
+    del rt
+    torch.cuda.empty_cache()
+    return {"value": B * w.max_new / (ms / 1000.0), "unit": "tokens/s", "ms_per_run": ms,
+            "algorithmic_bytes_per_run": nbytes, "decode_hbm_gbs": (nbytes / 1e9) / (ms / 1000.0),
+            "what": "same schedule and kernels, reserved-token control flow: one more micro step per short group"}
+
+
 def head_mode_run(w: Workload, prompts, conf: float) -> dict:
     """Model-driven groups: the stop head's logit against ln((1-c)/c).  The
     number of macro-steps is found by an untimed run, then one run is timed."""
@@ -216,6 +252,8 @@ def main() -> int:
                     help="first run one plain device-to-device copy of this size (HBM counter calibration)")
     ap.add_argument("--base", choices=("auto", "on", "off"), default="auto",
                     help="also time the same model decoding one token per forward (groups of one; auto: prompts <= 4096)")
+    ap.add_argument("--token-cost", action="store_true",
+                    help="also time the same schedule with the reserved-token stop variant (one more micro step per short group)")
     ap.add_argument("--graph", choices=("on", "off"), default="on",
                     help="replay each macro-step's launches from a HIP graph (on) or launch them on the stream")
     ap.add_argument("--head-sweep", default="",
@@ -347,6 +385,10 @@ def main() -> int:
     if args.base == "on" or (args.base == "auto" and P <= 4096 and not truncated):
         out["base_comparator"] = base_comparator(w, prompts, args.warmup, args.steps)
         out["speedup_vs_base"] = value / out["base_comparator"]["value"]
+    if args.token_cost and not truncated:
+        out["token_variant"] = token_cost_run(w, prompts, sched, lens, n_steps, args.warmup, args.steps)
+        out["token_variant"]["slowdown_vs_stop_head"] = value / out["token_variant"]["value"]
+        out["token_variant"]["bytes_ratio_vs_stop_head"] = out["token_variant"]["algorithmic_bytes_per_run"] / alg_bytes
     if args.head_sweep:
         out["head_sweep"] = [head_mode_run(w, prompts, float(c)) for c in args.head_sweep.split(",")]
     if args.cpu_steps > 0:

@@ -48,10 +48,17 @@ extern "C" {
  *  TOKEN  — the reserved-token variant: at micro index k >= 1, a predicted
  *           stop_id ends the group and is not emitted.
  *  FORCED — the group length is given per step by the caller (benchmarks and
- *           parity tests on random-initialised models). */
+ *           parity tests on random-initialised models); the group ends on the
+ *           decision that emits its last token, as with the stop head.
+ *  FORCED_TOKEN — FORCED lengths with the reserved-token variant's control
+ *           flow (Sec. 4.4): a group of L < max_group tokens ends on one more
+ *           micro step, decision k = L (k >= 1), taken as the reserved id and
+ *           not emitted.  Emits the same tokens as FORCED; measures the cost of
+ *           that extra step against the stop head. */
 #define HAM_STOP_HEAD 0
 #define HAM_STOP_TOKEN 1
 #define HAM_STOP_FORCED 2
+#define HAM_STOP_FORCED_TOKEN 3
 
 typedef struct ham_config {
   /* base decoder (Llama family: RMSNorm, RoPE, GQA, SwiGLU; Sec. 4.1) */
@@ -111,10 +118,10 @@ int ham_init_weights(const ham_config* cfg, uint64_t seed, void* d_weights, size
  * loop, which emit group 1 of every sequence.
  *  d_prompt      int32 [batch][prompt_len]
  *  h_max_new     int32 [batch] output-token budget per sequence (0 = none)
- *  d_forced_lens int32 [batch] group lengths for this step (FORCED mode only,
+ *  d_forced_lens int32 [batch] group lengths for this step (FORCED and FORCED_TOKEN modes only,
  *                otherwise may be NULL)
  *  d_teacher     int32 [batch][4] or NULL: teacher forcing for parity tests
- *                (FORCED mode only): the group fed back to the model is the
+ *                (FORCED modes only): the group fed back to the model is the
  *                teacher's tokens, while d_out_tokens still reports the
  *                model's own argmax at each position
  *  d_out_tokens  int32 [batch][4] the emitted group, d_out_lens int32 [batch]

@@ -18,7 +18,7 @@ from typing import Callable, List, Optional, Sequence
 import numpy as np
 
 import synth
-from synth.configs import BF16, STOP_FORCED, STOP_HEAD, STOP_TOKEN, HamShape
+from synth.configs import BF16, STOP_FORCED, STOP_FORCED_TOKEN, STOP_HEAD, STOP_TOKEN, HamShape
 
 
 # ----------------------------------------------------------------------------
@@ -317,6 +317,8 @@ class OracleHam:
             decisions.append(Decision(step, k, t, st, h if record else None, lg))
             if s.stop_mode == STOP_TOKEN and t == s.stop_id:
                 break  # reserved stop token: not emitted (Sec. 4.4 variant)
+            if s.stop_mode == STOP_FORCED_TOKEN and k >= forced_len:
+                break  # the forced length's reserved-token decision: not emitted (Sec. 4.4 variant)
             group.append(t)
             emitted += 1
             if (self._stop_after(k, st, forced_len) or len(group) >= G

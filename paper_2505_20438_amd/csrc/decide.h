@@ -6,13 +6,14 @@
 
 namespace ham {
 
-enum { STOP_HEAD = 0, STOP_TOKEN = 1, STOP_FORCED = 2 };
+enum { STOP_HEAD = 0, STOP_TOKEN = 1, STOP_FORCED = 2, STOP_FORCED_TOKEN = 3 };
 
 // Decision k of sequence b: greedy token t (lowest id among equal maxima) and
 // stop logit s.  Appends the token (the teacher's under teacher forcing) to the
 // group, then ends the group if the stop test fires, the group is full, or the
 // budget is spent.  In TOKEN mode a reserved id at k >= 1 ends the group and is
-// not emitted.  Finished groups update the counters used by ham_kv_stats.
+// not emitted; FORCED_TOKEN takes decision k = forced length (k >= 1) as that
+// id.  Finished groups update the counters used by ham_kv_stats.
 __device__ inline void decide_one(const DecideArgs& d, int b, int t, float s) {
   const SeqPtrs& st = d.st;
   if (!st.active[b]) return;
@@ -20,7 +21,8 @@ __device__ inline void decide_one(const DecideArgs& d, int b, int t, float s) {
   d.out_tokens[b * 4 + k] = t;
   if (d.dbg_stop) d.dbg_stop[b] = s;
   bool finish;
-  if (d.mode == STOP_TOKEN && k >= 1 && t == d.stop_id) {
+  if ((d.mode == STOP_TOKEN && k >= 1 && t == d.stop_id) ||
+      (d.mode == STOP_FORCED_TOKEN && k >= 1 && k >= st.forced[b])) {
     finish = true;
   } else {
     int tin = d.has_teacher ? st.teacher[b * 4 + k] : t;

@@ -87,7 +87,7 @@ const char* check_cfg(const ham_config* c) {
   if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32 || c->ffn_dim % 32) return "d_model, n_heads*head_dim and ffn_dim must be multiples of 32";
   if (c->d_model > 8192) return "d_model must be <= 8192";
   if (c->max_group < 1 || c->max_group > 4) return "max_group must be in 1..4";
-  if (c->stop_mode < 0 || c->stop_mode > 2) return "unknown stop_mode";
+  if (c->stop_mode < 0 || c->stop_mode > 3) return "unknown stop_mode";
   if (c->stop_mode == HAM_STOP_TOKEN && (c->stop_id < 0 || c->stop_id >= c->vocab)) return "stop_id out of range";
   if (!(c->stop_conf >= 0.f && c->stop_conf <= 1.f)) return "stop_conf must be in [0, 1]";
   if (c->dtype != HAM_F32 && c->dtype != HAM_BF16) return "dtype must be HAM_F32 or HAM_BF16";
@@ -738,8 +738,9 @@ int prefill_common(ham_model* m, int32_t batch, int32_t T, const int32_t* d_prom
                    const int32_t* d_positions, const int32_t* h_max_new, const int32_t* d_forced_lens,
                    const int32_t* d_teacher, int32_t* d_out_tokens, int32_t* d_out_lens) {
   const Layout& y = m->y;
-  if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
-  if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
+  const bool forced_mode = m->cfg.stop_mode == HAM_STOP_FORCED || m->cfg.stop_mode == HAM_STOP_FORCED_TOKEN;
+  if (forced_mode && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
+  if (d_teacher && !forced_mode) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
   for (int b = 0; b < batch; ++b)
     if (h_max_new[b] < 0) return fail(HAM_EINVAL, "negative budget");
   const int dt = dtype_of(m);
@@ -903,8 +904,9 @@ int ham_macro_step(ham_model* m, const int32_t* d_forced_lens, const int32_t* d_
   if (m->steps_done >= y.steps) return fail(HAM_ECAP, "max_steps (%d) reached", y.steps);
   if (m->prompt_len + m->steps_done + 1 > y.S)
     return fail(HAM_ECAP, "KV slot capacity (%d) reached", y.S);
-  if (m->cfg.stop_mode == HAM_STOP_FORCED && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
-  if (d_teacher && m->cfg.stop_mode != HAM_STOP_FORCED) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
+  const bool forced_mode = m->cfg.stop_mode == HAM_STOP_FORCED || m->cfg.stop_mode == HAM_STOP_FORCED_TOKEN;
+  if (forced_mode && !d_forced_lens) return fail(HAM_EINVAL, "FORCED mode needs forced lengths");
+  if (d_teacher && !forced_mode) return fail(HAM_EINVAL, "teacher forcing needs FORCED mode");
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
   const int B = m->batch;

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libham.so")
 
 HAM_OK, HAM_EINVAL, HAM_ENOMEM, HAM_EHIP, HAM_ESTATE, HAM_ECAP = 0, -1, -2, -3, -4, -5
 HAM_F32, HAM_BF16 = 0, 1
-HAM_STOP_HEAD, HAM_STOP_TOKEN, HAM_STOP_FORCED = 0, 1, 2
+HAM_STOP_HEAD, HAM_STOP_TOKEN, HAM_STOP_FORCED, HAM_STOP_FORCED_TOKEN = 0, 1, 2, 3
 
 HAM_PROF_KINDS = 9
 

@@ -11,7 +11,7 @@ from __future__ import annotations
 import dataclasses
 import math
 
-STOP_HEAD, STOP_TOKEN, STOP_FORCED = 0, 1, 2
+STOP_HEAD, STOP_TOKEN, STOP_FORCED, STOP_FORCED_TOKEN = 0, 1, 2, 3
 F32, BF16 = 0, 1
 
 

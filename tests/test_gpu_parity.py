@@ -9,7 +9,7 @@ import pytest
 
 import synth
 from oracle import OracleHam
-from synth.configs import BF16, SHAPE_1B, STOP_FORCED, STOP_HEAD, STOP_TOKEN, TINY, WORKLOADS
+from synth.configs import BF16, SHAPE_1B, STOP_FORCED, STOP_FORCED_TOKEN, STOP_HEAD, STOP_TOKEN, TINY, WORKLOADS
 from tests.gpu_util import SMALL16, TOL, check_decision, config_for, oracle_groups_for, run_gpu
 
 pytestmark = pytest.mark.gpu
@@ -59,7 +59,7 @@ def test_weights_match_generator_bf16_1b_sample(torch_cuda):
         assert np.mean(got != want) < 1e-4, tid
 
 
-@pytest.mark.parametrize("mode", ["c1", "head", "forced"])
+@pytest.mark.parametrize("mode", ["c1", "head", "forced", "forced_token"])
 def test_tiny_fp32_free_running_exact(torch_cuda, mode):
     # configuration 1: fp32, TOKEN stop id 1023, 64-token prompt, 128 macro-steps, no budget;
     # plus HEAD (c = 0.5) and FORCED variants on the same weights
@@ -68,8 +68,8 @@ def test_tiny_fp32_free_running_exact(torch_cuda, mode):
     sched = None
     if mode == "head":
         shp = dataclasses.replace(shp, stop_mode=STOP_HEAD, stop_conf=0.5)
-    elif mode == "forced":
-        shp = dataclasses.replace(shp, stop_mode=STOP_FORCED)
+    elif mode in ("forced", "forced_token"):
+        shp = dataclasses.replace(shp, stop_mode=STOP_FORCED if mode == "forced" else STOP_FORCED_TOKEN)
         sched = synth.group_schedule(w.seed_sched, 1, w.macro_steps + 1, 4)
     prompts = synth.prompt_ids(w.seed_prompt, 1, w.prompt_len, shp.vocab)
     om = OracleHam(shp, w.seed_weights)

@@ -13,7 +13,7 @@ import torch
 
 import synth
 from oracle import OracleHam
-from synth.configs import BF16, STOP_FORCED, STOP_HEAD, STOP_TOKEN, TINY
+from synth.configs import BF16, STOP_FORCED, STOP_FORCED_TOKEN, STOP_HEAD, STOP_TOKEN, TINY
 from tests.ref_torch import RefHam, plain_greedy
 
 SMALL = dataclasses.replace(TINY, vocab=96, d_model=64, n_heads=4, n_kv_heads=2, head_dim=16, ffn_dim=96,
@@ -138,3 +138,23 @@ def test_positions_advance_by_group_size():
     pos = np.concatenate([p for _, p in inputs])
     assert list(pos[:8]) == list(range(8))
     assert list(np.diff(pos[7:])) == [len(g) for g in res.groups[:-1]]
+
+
+def test_forced_token_costs_one_extra_micro_step_per_short_group():
+    # the reserved-token variant (Sec. 4.4) on forced lengths: the same groups as the
+    # stop-head control flow, plus one discarded decision for every group shorter than
+    # the cap (a group of one needs a micro step it would otherwise skip)
+    sched = synth.group_schedule(57, 1, 40, 4)[0]
+    prompt = _prompt(58, 12, SMALL.vocab)
+    res = {}
+    for mode in (STOP_FORCED, STOP_FORCED_TOKEN):
+        om = OracleHam(dataclasses.replace(SMALL, stop_mode=mode), 37)
+        res[mode] = om.generate(prompt, 0, 30, forced=lambda st: int(sched[st]))
+    head, tok = res[STOP_FORCED], res[STOP_FORCED_TOKEN]
+    assert tok.groups == head.groups and tok.kv_len == head.kv_len
+    assert [len(g) for g in head.groups] == [int(x) for x in sched[:31]]
+    extra = sum(1 for g in head.groups if len(g) < 4)
+    assert extra > 5
+    assert len(tok.decisions) == len(head.decisions) + extra
+    for g, n_dec in zip(head.groups, np.bincount([d.step for d in tok.decisions])):
+        assert n_dec == len(g) + (1 if len(g) < 4 else 0)

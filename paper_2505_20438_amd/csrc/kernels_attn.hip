@@ -58,7 +58,9 @@ struct KVBlock {
   u4 v[ND];
 };
 
-template <typename T, int HD>
+// NT: non-temporal loads (decode reads every block once); prefill re-reads each
+// block from many waves, so it keeps them cacheable.
+template <typename T, int HD, bool NT = true>
 __device__ __forceinline__ void kv_load(KVBlock<T, HD>& blk, const T* Kb, const T* Vb, int S, int base) {
   using B = KVBlock<T, HD>;
   constexpr int EPL = Frag<T>::EPL, KB = B::KB;
@@ -69,12 +71,13 @@ __device__ __forceinline__ void kv_load(KVBlock<T, HD>& blk, const T* Kb, const 
     const int slot = base + (r16 >> 2) * (KB / 4) + 4 * t + (r16 & 3);
     const T* kp = Kb + (size_t)slot * HD + g * EPL;
 #pragma unroll
-    for (int f = 0; f < B::NF; ++f) blk.k[t][f] = ld16_stream(kp + f * KB);
+    for (int f = 0; f < B::NF; ++f) blk.k[t][f] = NT ? ld16_stream(kp + f * KB) : ld16(kp + f * KB);
   }
   // V^T row d = dt*16 + r16 of the block's tile, slots base + g*KB/4 .. (KB <= 32 stays inside one tile)
   const T* vp = Vb + vt_offset(r16, base, HD) + g * (KB / 4);
 #pragma unroll
-  for (int dt = 0; dt < B::ND; ++dt) blk.v[dt] = ld16_stream(vp + (size_t)dt * 16 * VT_TILE);
+  for (int dt = 0; dt < B::ND; ++dt)
+    blk.v[dt] = NT ? ld16_stream(vp + (size_t)dt * 16 * VT_TILE) : ld16(vp + (size_t)dt * 16 * VT_TILE);
 }
 
 // Keep the first `keep` elements of a lane fragment, zero the rest.
@@ -157,7 +160,7 @@ template <int HD> struct AttnChunk { static constexpr int NB = 256 / HD; };
 // Key blocks [b0, b1) of KB slots from slot0, masked at `limit` / `vlimit`.
 // The blocks go in chunks of NB whose loads are all issued before any of them
 // is used, so a chunk costs one memory round trip.
-template <typename T, int HD>
+template <typename T, int HD, bool NT = true>
 __device__ __forceinline__ void attn_blocks(const T* Kb, const T* Vb, int S, int slot0, int b0, int b1, int limit,
                                             int vlimit, const u4* qf, const u4* ql, float scale, float& mrun,
                                             float& lrun, f4* o) {
@@ -166,7 +169,7 @@ __device__ __forceinline__ void attn_blocks(const T* Kb, const T* Vb, int S, int
     KVBlock<T, HD> blk[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      if (c + i < b1) kv_load<T, HD>(blk[i], Kb, Vb, S, slot0 + (c + i) * KB);
+      if (c + i < b1) kv_load<T, HD, NT>(blk[i], Kb, Vb, S, slot0 + (c + i) * KB);
 #pragma unroll
     for (int i = 0; i < NB; ++i)
       if (c + i < b1) attn_block<T, HD>(blk[i], slot0 + (c + i) * KB, limit, vlimit, qf, ql, scale, mrun, lrun, o);
@@ -554,7 +557,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
   // per-lane limit: the score mask uses this lane's query row (r16)
-  attn_blocks<T, HD>(Kb, Vb, a.S, 0, 0, (wave_end + KB - 1) / KB, limit, wave_end, qf, ql, scale, mrun, lrun, o);
+  attn_blocks<T, HD, false>(Kb, Vb, a.S, 0, 0, (wave_end + KB - 1) / KB, limit, wave_end, qf, ql, scale, mrun, lrun,
+                            o);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int j = 4 * g + i;  // query row within the wave

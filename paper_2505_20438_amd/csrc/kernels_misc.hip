@@ -153,52 +153,82 @@ int launch_rope_append(int dtype, const RopeArgs& a, Stream s) {
 // Sec. 3.2), take the next KV slot, and open a new group.
 template <typename T>
 __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
-  __shared__ int tok[4];
-  __shared__ int sn, son, spos;
-  const int b = blockIdx.x;
+  __shared__ int sh[7];  // n, on, new position, tokens 0..3
+  const int b = blockIdx.x, tid = threadIdx.x;
   const SeqPtrs& st = a.st;
-  if (threadIdx.x == 0) {
-    const int on = st.done[b] ? 0 : 1;
-    const int n = st.grp_n[b];
-    sn = n;
-    son = on;
-    for (int j = 0; j < 4; ++j) tok[j] = j < n ? st.grp_tok[b * 4 + j] : 0;
+  if (tid == 0) {  // every state word in one round trip (tokens past the group are not used)
+    const int done = st.done[b], n = st.grp_n[b], pl = st.pos_last[b];
+    int t[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) t[j] = st.grp_tok[b * 4 + j];
+    sh[0] = n;
+    sh[1] = done ? 0 : 1;
+    sh[2] = pl + n;  // the fused input sits at its group's last token's position
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sh[3 + j] = j < n ? t[j] : 0;
   }
   __syncthreads();
-  const int n = sn, on = son;
-  const int d = a.d;
+  const int n = sh[0], on = sh[1], p = sh[2];
+  const int spos = on ? min(max(p, 0), a.max_pos - 1) : -1;
+  const int d = a.d, half = a.hd / 2;
   const T* E = (const T*)a.E;
   const T* P = (const T*)a.P;
-  if (on && n == 1) {
-    for (int i = threadIdx.x; i < d; i += 256) a.x[(size_t)b * a.ldx + i] = to_f<T>(E[(size_t)tok[0] * d + i]);
+  // RoPE factors of this step's base input (read by every layer's attention step),
+  // loaded together with the embedding rows
+  if (spos >= 0)
+    for (int i = tid; i < half; i += 256) {
+      a.rope_cs[(size_t)b * a.hd + i] = a.cos_t[(size_t)spos * half + i];
+      a.rope_cs[(size_t)b * a.hd + half + i] = a.sin_t[(size_t)spos * half + i];
+    }
+  if (on && n == 1) {  // bypass: the single token's embedding is the base input
+    constexpr int U = 8;
+    const T* er = E + (size_t)sh[3] * d;
+    for (int i0 = tid; i0 < d; i0 += 256 * U) {
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = i0 + 256 * u < d ? to_f<T>(er[i0 + 256 * u]) : 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i0 + 256 * u < d) a.x[(size_t)b * a.ldx + i0 + 256 * u] = v[u];
+    }
   } else if (on && n > 1) {
     // e_j = E[t_j] + P[j]; query = mean_j e_j; rows of the embedder's projection GEMM
-    for (int i = threadIdx.x; i < d; i += 256) {
-      float sum = 0.f;
-      for (int j = 0; j < 4; ++j) {
-        float e = 0.f;
-        if (j < n) {
-          e = to_f<T>(E[(size_t)tok[j] * d + i]) + to_f<T>(P[(size_t)j * d + i]);
-          sum += e;
+    constexpr int U = 2;
+    for (int i0 = tid; i0 < d; i0 += 256 * U) {
+      float ev[U][4], pv[U][4];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = i0 + 256 * u;
+          const bool ok = i < d && j < n;
+          ev[u][j] = ok ? to_f<T>(E[(size_t)sh[3 + j] * d + i]) : 0.f;
+          pv[u][j] = ok ? to_f<T>(P[(size_t)j * d + i]) : 0.f;
         }
-        Act<T>::put(a.emb_in, (size_t)b * 5 + 1 + j, d, i, e);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + 256 * u;
+        if (i >= d) continue;
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float e = j < n ? ev[u][j] + pv[u][j] : 0.f;
+          sum += e;
+          Act<T>::put(a.emb_in, (size_t)b * 5 + 1 + j, d, i, e);
+        }
+        Act<T>::put(a.emb_in, (size_t)b * 5, d, i, sum / (float)n);
       }
-      Act<T>::put(a.emb_in, (size_t)b * 5, d, i, sum / (float)n);
     }
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     st.step_on[b] = on;
     st.fused[b] = (on && n > 1) ? n : 0;
-    spos = -1;
     if (on) {
-      const int p = st.pos_last[b] + n;
       st.pos_last[b] = p;
       st.cur_pos[b] = p;
       st.cur_slot[b] = st.kv_len[b];
       st.kv_len[b] += 1;
       if (p < 0 || p >= a.max_pos) atomicOr(st.err + b, 1);
-      spos = min(max(p, 0), a.max_pos - 1);
     }
     st.forced[b] = a.forced_in ? a.forced_in[b] : a.G;
     for (int j = 0; j < 4; ++j) {
@@ -209,15 +239,6 @@ __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
     st.grp_n[b] = 0;
     st.active[b] = on;
   }
-  // RoPE factors of this step's base input, read by every layer's attention step
-  __syncthreads();
-  const int half = a.hd / 2;
-  if (spos >= 0) {
-    for (int i = threadIdx.x; i < half; i += 256) {
-      a.rope_cs[(size_t)b * a.hd + i] = a.cos_t[(size_t)spos * half + i];
-      a.rope_cs[(size_t)b * a.hd + half + i] = a.sin_t[(size_t)spos * half + i];
-    }
-  }
 }
 
 // Embedder attention over the <= 4 token rows of a fused group: per head, the
@@ -225,42 +246,57 @@ __global__ __launch_bounds__(256) void k_macro_begin(MacroArgs a) {
 // (row 0 query, rows 1..4 tokens; columns Q | K | V).
 template <typename T>
 __global__ __launch_bounds__(64) void k_embed_attn(EmbedAttnArgs a) {
-  const int b = blockIdx.x, h = blockIdx.y;
+  const int b = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int n = a.fused[b];
   if (n < 2) return;
   const int hd = a.hd, HD = a.H * a.hd;  // proj row: Q | K | V blocks of H*hd each
-  // projection value (row, col), summing split-K partials when present
-  auto P = [&](int row, int col) {
-    const size_t idx = ((size_t)b * 5 + row) * 3 * HD + col;
-    if (!a.part) return a.proj[idx];
-    float v = 0.f;
-    for (int s = 0; s < a.nsplit; ++s) v += a.part[(size_t)s * a.B * 5 * 3 * HD + idx];
-    return v;
-  };
-  __shared__ float w[4];
-  __shared__ float qs[128];
-  for (int i = threadIdx.x; i < hd; i += 64) qs[i] = P(0, h * hd + i);
-  __syncthreads();
-  if (threadIdx.x < 4) {
-    const int j = threadIdx.x;
-    float s = -INFINITY;
-    if (j < n) {
-      s = 0.f;
-      for (int i = 0; i < hd; ++i) s += qs[i] * P(1 + j, HD + h * hd + i);
-      s *= 1.0f / sqrtf((float)hd);
+  // lane holds elements lane and lane + 64 of the head: the query, the n keys and
+  // values, each summed over the split-K partials (one load of every value per split)
+  constexpr int NE = 2;  // hd <= 128
+  const int ns = a.part ? a.nsplit : 1;
+  const float* src = a.part ? a.part : a.proj;
+  const size_t sstride = (size_t)a.B * 5 * 3 * HD;
+  float q[NE] = {}, k[4][NE] = {}, v[4][NE] = {};
+  for (int sp = 0; sp < ns; ++sp) {
+    const float* base = src + (size_t)sp * sstride + (size_t)b * 5 * 3 * HD + (size_t)h * hd;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const int i = lane + 64 * e;
+      if (i >= hd) continue;
+      q[e] += base[i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (j < n) {
+          k[j][e] += base[(size_t)(1 + j) * 3 * HD + HD + i];
+          v[j][e] += base[(size_t)(1 + j) * 3 * HD + 2 * HD + i];
+        }
     }
-    w[j] = s;
   }
-  __syncthreads();
-  float m = fmaxf(fmaxf(w[0], w[1]), fmaxf(w[2], w[3]));
-  float e[4], sum = 0.f;
+  float w[4];
+  float m = -INFINITY;
+#pragma unroll
   for (int j = 0; j < 4; ++j) {
-    e[j] = j < n ? expf(w[j] - m) : 0.f;
-    sum += e[j];
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) s += q[e] * k[j][e];
+    s = wave_sum(s) * (1.0f / sqrtf((float)hd));
+    w[j] = j < n ? s : -INFINITY;
+    m = fmaxf(m, w[j]);
   }
-  for (int i = threadIdx.x; i < hd; i += 64) {
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    w[j] = j < n ? expf(w[j] - m) : 0.f;
+    sum += w[j];
+  }
+#pragma unroll
+  for (int e = 0; e < NE; ++e) {
+    const int i = lane + 64 * e;
+    if (i >= hd) continue;
     float acc = 0.f;
-    for (int j = 0; j < n; ++j) acc += e[j] * P(1 + j, 2 * HD + h * hd + i);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j < n) acc += w[j] * v[j][e];
     Act<T>::put(a.out, b, HD, h * hd + i, acc / sum);
   }
 }

@@ -16,7 +16,8 @@
 //   write (max, sum, unnormalised output) and k_attn_combine merges them with
 //   the log-sum-exp rule in split order.  Used for base decode (ragged kv_len per sequence) and the micro
 //   decoder's local cache.
-// k_attn_prefill: four waves of 16 consecutive query rows of one head, causal.
+// k_attn_prefill: the q-heads of a kv head over 16-row groups of a prompt chunk,
+//   key blocks shared through LDS, causal.
 //
 // Softmax statistics are fp32.  For bf16 caches the probabilities enter the
 // bf16 product as a hi + lo pair (about 16 significant bits).
@@ -527,46 +528,136 @@ __global__ __launch_bounds__(COMBINE_THREADS) void k_attn_combine(AttnArgs a) {
   }
 }
 
+// Prefill: causal attention of a prompt chunk (rows of mode PREFILL: slots
+// t0 + r of one sequence).  One workgroup of PF_NW waves per (row chunk, kv
+// head): wave w takes q-head kvh*grp + w % grp and the 16 rows 16*(w / grp)..
+// of the chunk, so a chunk is 16*(PF_NW / grp) rows.  The key blocks pass
+// through LDS once per workgroup, PF_NBL blocks per stage, double-buffered:
+// the global loads are contiguous, and each 16-byte piece is stored where a
+// wave's operand fragment expects it (K as [tile][fragment][lane], V^T as
+// [d-tile][lane]), so every operand read of a wave is one contiguous 1 KB.
+constexpr int PF_NW = 8, PF_NBL = 2;
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void k_attn_prefill(AttnArgs a) {
-  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, NF = HD / KB, ND = HD / 16;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
-  const int h = blockIdx.y;
-  const int grp = a.H / a.Hkv, kvh = h / grp;
-  const int row0 = blockIdx.x * 64 + w * 16;
-  if (row0 >= a.R) return;
-  const RowInfo r0 = row_info(a.rm, row0);
+struct PrefillBlock {  // 16-byte pieces of one key block: K, then V
+  static constexpr int KB = Frag<T>::KB, EPL = Frag<T>::EPL, NF = HD / KB, ND = HD / 16, TT = KB / 16;
+  static constexpr int KU = TT * NF * 64, VU = ND * 64, BU = KU + VU;
+};
+
+template <typename T, int HD>
+__global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
+  using PB = PrefillBlock<T, HD>;
+  constexpr int KB = PB::KB, EPL = PB::EPL, NF = PB::NF, ND = PB::ND, TT = PB::TT, KU = PB::KU, BU = PB::BU;
+  constexpr int SU = PF_NBL * BU;                          // pieces per stage
+  constexpr int PER = (SU + 64 * PF_NW - 1) / (64 * PF_NW);  // pieces per thread per stage
+  __shared__ u4 lds[2][SU];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int kvh = blockIdx.y;
+  const int grp = a.H / a.Hkv, nrg = PF_NW / grp, RB = 16 * nrg;
+  const int jh = w % grp, rg = w / grp;
+  const int h = kvh * grp + jh;
+  const int chunk0 = blockIdx.x * RB;
+  if (chunk0 >= a.R) return;  // the same for every wave of the workgroup
+  const RowInfo r0 = row_info(a.rm, chunk0);
+  const int wg_end = r0.slot + min(RB, a.R - chunk0);  // keys [0, wg_end)
+  const int row0 = chunk0 + rg * 16;
+  const bool rows_ok = rg < nrg && row0 < a.R;          // waves past the q-heads only load
+  const int wave_end = rows_ok ? r0.slot + (row0 - chunk0) + min(16, a.R - row0) : 0;
   const T* Kb = (const T*)a.K + r0.b * a.sb + kvh * a.sh;
   const T* Vb = (const T*)a.VT + r0.b * a.sb + kvh * a.sh;
+
   const int qrow = row0 + r16;
-  const bool qok = qrow < a.R;
+  const bool qok = rows_ok && qrow < a.R;
   u4 qf[NF], ql[NF];
   constexpr int PL = Act<T>::PL;
-  const T* qp = (const T*)a.q + (size_t)(qok ? qrow : row0) * a.ldq * PL + (size_t)h * HD + g * EPL;
+  const T* qp = (const T*)a.q + (size_t)(qok ? qrow : 0) * a.ldq * PL + (size_t)h * HD + g * EPL;
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     qf[f] = qok ? ld16(qp + f * KB) : zero16();
     ql[f] = (Act<T>::SPLIT && qok) ? ld16(qp + a.ldq + f * KB) : zero16();
   }
-  // causal: row with slot s sees slots [0, s]; rows past the chunk see nothing
-  const int limit = qok ? r0.slot + r16 + 1 : 0;
-  const int wave_end = r0.slot + min(15, a.R - 1 - row0) + 1;
+  // causal: the row at slot s sees slots [0, s]
+  const int limit = qok ? r0.slot + (qrow - chunk0) + 1 : 0;
+
+  const int nblk = (wg_end + KB - 1) / KB, nst = (nblk + PF_NBL - 1) / PF_NBL;
+  // piece c of a key block: global source and LDS position
+  auto src_of = [&](int blk, int c) -> const T* {
+    const int base = blk * KB;
+    if (c < KU) {
+      const int sl = c / (HD / EPL), cc = c % (HD / EPL);
+      return Kb + (size_t)(base + sl) * HD + cc * EPL;
+    }
+    c -= KU;
+    return Vb + vt_offset(c / 4, base, HD) + (c % 4) * (KB / 4);
+  };
+  auto dst_of = [&](int c) -> int {
+    if (c < KU) {
+      // slot sl of the block is operand row 4*(sl / (KB/4)) + sl % 4 of tile (sl % (KB/4)) / 4
+      const int sl = c / (HD / EPL), col = (c % (HD / EPL)) * EPL;
+      const int qq = KB / 4, t = (sl % qq) / 4, rr = 4 * (sl / qq) + sl % 4;
+      return (t * NF + col / KB) * 64 + ((col % KB) / EPL) * 16 + rr;
+    }
+    c -= KU;
+    const int d = c / 4;
+    return KU + (d / 16) * 64 + (c % 4) * 16 + d % 16;
+  };
+  u4 sr[PER];
+  auto gload = [&](int stg) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int q = tid + k * 64 * PF_NW;
+      const int blk = stg * PF_NBL + q / BU;
+      if (q < SU && blk < nblk) sr[k] = ld16(src_of(blk, q % BU));
+    }
+  };
+  auto lstore = [&](int stg, int buf) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int q = tid + k * 64 * PF_NW;
+      const int blk = stg * PF_NBL + q / BU;
+      if (q < SU && blk < nblk) lds[buf][(q / BU) * BU + dst_of(q % BU)] = sr[k];
+    }
+  };
+
   f4 o[ND];
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
   const float scale = 1.0f / sqrtf((float)HD);
-  // per-lane limit: the score mask uses this lane's query row (r16)
-  attn_blocks<T, HD, false>(Kb, Vb, a.S, 0, 0, (wave_end + KB - 1) / KB, limit, wave_end, qf, ql, scale, mrun, lrun,
-                            o);
+  if (nst > 0) {
+    gload(0);
+    lstore(0, 0);
+  }
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nst) gload(st + 1);  // in flight while this stage is used
+#pragma unroll
+    for (int i = 0; i < PF_NBL; ++i) {
+      const int blk = st * PF_NBL + i;
+      if (blk < nblk && blk * KB < wave_end) {  // blocks past this wave's last row hold nothing it sees
+        KVBlock<T, HD> kv;
+        const u4* bp = &lds[buf][i * BU];
+#pragma unroll
+        for (int t = 0; t < TT; ++t)
+#pragma unroll
+          for (int f = 0; f < NF; ++f) kv.k[t][f] = bp[(t * NF + f) * 64 + lane];
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) kv.v[dt] = bp[KU + dt * 64 + lane];
+        attn_block<T, HD>(kv, blk * KB, limit, wave_end, qf, ql, scale, mrun, lrun, o);
+      }
+    }
+    if (st + 1 < nst) lstore(st + 1, buf ^ 1);  // the other buffer was last read before the previous barrier
+    __syncthreads();
+  }
+  if (!rows_ok) return;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int j = 4 * g + i;  // query row within the wave
-    const float lj = __shfl(lrun, j, WAVE);
-    if (row0 + j < a.R) {
+    const int jr = 4 * g + i;  // query row within the wave
+    const float lj = __shfl(lrun, jr, WAVE);
+    if (row0 + jr < a.R) {
       const float inv = lj > 0.f ? 1.0f / lj : 0.f;
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, row0 + j, a.ldo, h * HD + r16 + dt * 16, o[dt][i] * inv);
+      for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, row0 + jr, a.ldo, h * HD + r16 + dt * 16, o[dt][i] * inv);
     }
   }
 }
@@ -582,9 +673,12 @@ static int decode_t(const AttnArgs& a, Stream s) {
 }
 template <typename T>
 static int prefill_t(const AttnArgs& a, Stream s) {
-  dim3 grid((a.R + 63) / 64, a.H);
-  if (a.hd == 64) launch_k((k_attn_prefill<T, 64>), grid, dim3(256), 0, s, a);
-  else if (a.hd == 128) launch_k((k_attn_prefill<T, 128>), grid, dim3(256), 0, s, a);
+  const int grp = a.H / a.Hkv;
+  if (grp < 1 || grp > PF_NW) return -1;
+  const int rb = 16 * (PF_NW / grp);  // rows per workgroup
+  dim3 grid((a.R + rb - 1) / rb, a.Hkv);
+  if (a.hd == 64) launch_k((k_attn_prefill<T, 64>), grid, dim3(64 * PF_NW), 0, s, a);
+  else if (a.hd == 128) launch_k((k_attn_prefill<T, 128>), grid, dim3(64 * PF_NW), 0, s, a);
   else return -1;
   return 0;
 }

@@ -73,7 +73,7 @@ struct Layout {
   // state
   size_t Kc, VTc, kv_layer, seq, st_bytes;
   // workspace
-  size_t x, x2, xp, xn, qkv, q, ao, act, part, qpart, ssb, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
+  size_t x, x2, xp, xn, qkv, q, ao, act, part, qpart, ssb, nss, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
       rope_cs, Kloc, VTloc, loc_layer, ws_bytes;
 };
 
@@ -161,6 +161,7 @@ Layout make_layout(const ham_config* c) {
   y.part = take((size_t)PART_ROWS * y.Nmax * 4);
   y.qpart = take((size_t)PART_ROWS * y.QKV * 4);  // q/k/v partials (read while part is pending)
   y.ssb = take((size_t)MAX_GEMM_SPLIT * 64 * 4);
+  y.nss = take((size_t)y.rows_max * ((y.d + 255) / 256) * 4);  // two-phase RMSNorm chunk sums
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);
   y.apart = take(attn_part_bytes(y.rows_dec, y.H, y.Hk, y.hd));
@@ -306,7 +307,7 @@ int norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* g
   na.x = x; na.ldx = y.d; na.row_stride = stride; na.row_off = off; na.g = g; na.d = y.d; na.R = R;
   na.eps = m->cfg.norm_eps; na.out = m->WS<char>(y.xn); na.ldo = y.d; na.hid = hid; na.ldh = y.d;
   na.part = pend.part; na.nsplit = pend.nsplit; na.pM = pend.M; na.ctx = ctx; na.ldctx = ldctx;
-  na.gate = gate; na.gate_n = gate_n;
+  na.gate = gate; na.gate_n = gate_n; na.ss = m->WS<float>(y.nss);
   pend = Pending{};
   return launch_rmsnorm(dtype_of(m), na, m->s) ? fail(HAM_EINVAL, "rmsnorm shape") : HAM_OK;
 }

@@ -193,6 +193,7 @@ struct NormArgs {
   void* out; int ldo;                                 // storage-type output
   float* hid; int ldh;                                // optional fp32 copy of the normed rows
   const int* gate; int gate_n;
+  float* ss;                                          // scratch [R][d/256] for the two-phase form, or null
 };
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s);
 

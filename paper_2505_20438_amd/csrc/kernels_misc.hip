@@ -82,9 +82,64 @@ __global__ __launch_bounds__(NORM_THREADS) void k_rmsnorm(NormArgs a) {
   }
 }
 
+// Two-phase form for batches of rows (one workgroup per row leaves most CUs
+// idle while it reads the pending partials): phase 1 over (256-column chunks,
+// rows) folds the partials into x and writes each chunk's sum of squares;
+// phase 2 sums a row's chunk sums in order and writes the scaled operand.
+constexpr int NORM2_MIN_ROWS = 16, NORM2_MAX_ROWS = 256;  // decode batches (prefill chunks fill the GPU already)
+__global__ __launch_bounds__(256) void k_norm_reduce(NormArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  __shared__ float sh4[4];
+  const int r = blockIdx.y, i = blockIdx.x * 256 + threadIdx.x;
+  const int xr = r * a.row_stride + a.row_off;
+  float* x = a.x + (size_t)xr * a.ldx;
+  float v = 0.f;
+  if (i < a.d) {
+    v = x[i];
+    if (a.part) {
+      const size_t sstride = (size_t)a.pM * a.ldx;
+      const float* pp = a.part + (size_t)xr * a.ldx + i;
+      float p[NORM_MAXS];
+#pragma unroll
+      for (int q = 0; q < NORM_MAXS; ++q)
+        if (q < a.nsplit) p[q] = pp[(size_t)q * sstride];
+#pragma unroll
+      for (int q = 0; q < NORM_MAXS; ++q)
+        if (q < a.nsplit) v += p[q];
+      x[i] = v;
+    }
+    if (a.ctx) a.ctx[(size_t)r * a.ldctx + i] = v;
+  }
+  const float ss = block_sum256(v * v, sh4);
+  if (threadIdx.x == 0) a.ss[(size_t)r * gridDim.x + blockIdx.x] = ss;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_norm_scale(NormArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  const int r = blockIdx.y, i = blockIdx.x * 256 + threadIdx.x, nch = gridDim.x;
+  const int xr = r * a.row_stride + a.row_off;
+  const float v = i < a.d ? a.x[(size_t)xr * a.ldx + i] : 0.f;
+  float tot = 0.f;
+  for (int c = 0; c < nch; ++c) tot += a.ss[(size_t)r * nch + c];
+  const float inv = 1.0f / sqrtf(tot / (float)a.d + a.eps);
+  if (i < a.d) {
+    const float o = v * inv * a.g[i];
+    Act<T>::put(a.out, r, a.ldo, i, o);
+    if (a.hid) a.hid[(size_t)r * a.ldh + i] = o;
+  }
+}
+
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
   if (a.R <= 0) return 0;
   if (a.d > NORM_THREADS * NORM_MAXV || (a.part && (a.nsplit < 1 || a.nsplit > NORM_MAXS))) return -1;
+  if (a.ss && a.R >= NORM2_MIN_ROWS && a.R <= NORM2_MAX_ROWS) {
+    const dim3 grid((a.d + 255) / 256, a.R);
+    launch_k(k_norm_reduce, grid, dim3(256), 0, s, a);
+    if (dtype == 1) launch_k((k_norm_scale<bf16>), grid, dim3(256), 0, s, a);
+    else launch_k((k_norm_scale<float>), grid, dim3(256), 0, s, a);
+    return 0;
+  }
   if (dtype == 1) launch_k((k_rmsnorm<bf16>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
   else launch_k((k_rmsnorm<float>), dim3(a.R), dim3(NORM_THREADS), 0, s, a);
   return 0;

@@ -23,7 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 import synth  # noqa: E402
-from synth.configs import BF16, WORKLOADS, Workload  # noqa: E402
+from synth.configs import BF16, STOP_FORCED, STOP_FORCED_TOKEN, WORKLOADS, Workload  # noqa: E402
 
 METRIC = "output tokens/s at 1 GPU; KV entries per output token; decode HBM GB/s"
 HBM_PEAK_GBS = 8000.0
@@ -269,25 +269,38 @@ def main() -> int:
 
     w = WORKLOADS[args.workload]
     s = w.shape
-    if w.max_new <= 0:
-        raise SystemExit("the benchmark needs a budgeted workload")
+    # unbudgeted workloads (the tiny fp32 model: TOKEN stop, 128 macro-steps) run
+    # a fixed number of macro-steps; their tokens are counted on the device
+    unbudgeted = w.max_new <= 0
+    forced_mode = s.stop_mode in (STOP_FORCED, STOP_FORCED_TOKEN)
     B, P = w.batch, w.prompt_len
     dev = torch.device("cuda:0")
     cfg = ham.make_config(n_layers=s.n_layers, d_model=s.d_model, n_heads=s.n_heads, n_kv_heads=s.n_kv_heads,
                           head_dim=s.head_dim, ffn_dim=s.ffn_dim, vocab=s.vocab, micro_layers=s.micro_layers,
                           max_group=s.max_group, stop_mode=s.stop_mode, stop_id=s.stop_id, dtype=s.dtype,
-                          max_batch=B, max_prompt=P, max_steps=w.max_new)
+                          max_batch=B, max_prompt=P, max_steps=w.macro_steps if unbudgeted else w.max_new)
     rt = ham.HamRuntime(cfg, w.seed_weights, "cuda:0")
     rt.set_graph(args.graph == "on")
     stream = rt.stream
     prompts = torch.from_numpy(synth.prompt_ids(w.seed_prompt, B, P, s.vocab)).to(dev)
-    sched_np = synth.group_schedule(w.seed_sched, B, w.max_new + 1, s.max_group)
-    sched = torch.from_numpy(np.ascontiguousarray(sched_np.T)).to(dev)   # [step][B], resident
-    budgets = [w.max_new] * B
-    lens = [group_lengths(sched_np[b], w.max_new) for b in range(B)]
-    n_steps = max(len(l) for l in lens) - 1
-    tokens_per_run = sum(budgets)
-    if args.max_macro_steps > 0 and args.max_macro_steps < n_steps:
+    n_sched = (w.macro_steps if unbudgeted else w.max_new) + 1
+    sched_np = synth.group_schedule(w.seed_sched, B, n_sched, s.max_group)
+    sched_dev = torch.from_numpy(np.ascontiguousarray(sched_np.T)).to(dev)   # [step][B], resident
+    sched = [sched_dev[st] if forced_mode else None for st in range(n_sched)]
+    budgets = [max(w.max_new, 0)] * B
+    if unbudgeted:
+        lens = None
+        n_steps = w.macro_steps
+        rt.prefill(prompts, budgets, sched[0])   # the prefill's group, excluded from the decode tokens
+        first = int(rt.out_lens[:B].sum())
+        for st in range(1, n_steps + 1):
+            rt.macro_step(sched[st])
+        tokens_per_run = sum(x["tokens"] for x in rt.kv_stats()) - first
+    else:
+        lens = [group_lengths(sched_np[b], w.max_new) for b in range(B)]
+        n_steps = max(len(l) for l in lens) - 1
+        tokens_per_run = sum(budgets)
+    if not unbudgeted and args.max_macro_steps > 0 and args.max_macro_steps < n_steps:
         n_steps = args.max_macro_steps   # profiler passes: the JSON line is then not a benchmark result
         tokens_per_run = sum(sum(l[:n_steps + 1]) for l in lens)
     if args.copy_calibration_mb > 0:
@@ -329,12 +342,16 @@ def main() -> int:
     wall = time.perf_counter() - t0
     dec_med = float(np.median(decode_ms))
     stats = rt.kv_stats()
-    truncated = n_steps < max(len(l) for l in lens) - 1
-    assert all((truncated or st["tokens"] == w.max_new) and st["device_error"] == 0 for st in stats), stats
+    truncated = (not unbudgeted) and n_steps < max(len(l) for l in lens) - 1
+    assert all((unbudgeted or truncated or st["tokens"] == w.max_new) and st["device_error"] == 0
+               for st in stats), stats
+    if unbudgeted:
+        assert sum(st["tokens"] for st in stats) - first == tokens_per_run   # deterministic across runs
     gen_slots = sum(st["gen_slots"] for st in stats)
     dec_ms = dec_med
     value = tokens_per_run / (dec_ms / 1000.0)
-    alg_bytes = algorithmic_bytes(w, lens, n_steps)
+    # the tiny model's 20 MB stay in the caches: no HBM bytes model for it
+    alg_bytes = None if unbudgeted else algorithmic_bytes(w, lens, n_steps)
 
     # per-kernel-class timing: one more run with HIP events attached to the
     # dispatch of every launch of the classes (same launch configuration, outside
@@ -355,6 +372,8 @@ def main() -> int:
     roofline = {"bound": "hbm", "achieved": kd["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": kd["gbs"] / HBM_PEAK_GBS, "traffic": None, "kernel": dom,
                 "bytes_per_launch": kd["bytes_per_launch"], "avg_us": kd["avg_us"]}
+    if unbudgeted:
+        roofline["note"] = "the tiny model stays in the on-chip caches: launch-latency bound, HBM fraction not meaningful"
     if dom == "gate_up":
         roofline["kernel_name"] = gate_up_kernel(w)
         roofline["traffic"] = measured_traffic(w, roofline["kernel_name"])
@@ -365,11 +384,13 @@ def main() -> int:
         "vs_baseline": None, "dtype": "bf16" if s.dtype == BF16 else "f32", "data": "synthetic",
         "config": {"workload": w.name, "batch": B, "prompt_len": P, "output_tokens_per_seq": w.max_new,
                    "layers": s.n_layers, "d_model": s.d_model, "micro_layers": s.micro_layers,
-                   "schedule": "forced geometric group lengths p=1/2, cap 4", "macro_steps": n_steps},
+                   "schedule": ("forced geometric group lengths p=1/2, cap 4" if forced_mode
+                                else f"model-driven stops (mode {s.stop_mode}, stop id {s.stop_id})"),
+                   "macro_steps": n_steps},
         "kv_entries_per_output_token": gen_slots / float(sum(st["tokens"] for st in stats)),
         "kv_entries_per_token_incl_prompt": (B * P + gen_slots) / float(B * P + sum(st["tokens"] for st in stats)),
-        "decode_hbm_gbs": (alg_bytes / 1e9) / (dec_ms / 1000.0),
-        "decode_hbm_frac": (alg_bytes / 1e9) / (dec_ms / 1000.0) / HBM_PEAK_GBS,
+        "decode_hbm_gbs": None if alg_bytes is None else (alg_bytes / 1e9) / (dec_ms / 1000.0),
+        "decode_hbm_frac": None if alg_bytes is None else (alg_bytes / 1e9) / (dec_ms / 1000.0) / HBM_PEAK_GBS,
         "algorithmic_bytes_per_run": alg_bytes,
         "prefill_ms": float(np.mean(prefill_ms)),
         "us_per_macro_step": 1000.0 * dec_ms / n_steps,
@@ -382,10 +403,10 @@ def main() -> int:
     out["decode_ms_runs"] = [float(x) for x in decode_ms]
     del rt
     torch.cuda.empty_cache()
-    if args.base == "on" or (args.base == "auto" and P <= 4096 and not truncated):
+    if not unbudgeted and (args.base == "on" or (args.base == "auto" and P <= 4096 and not truncated)):
         out["base_comparator"] = base_comparator(w, prompts, args.warmup, args.steps)
         out["speedup_vs_base"] = value / out["base_comparator"]["value"]
-    if args.token_cost and not truncated:
+    if args.token_cost and not truncated and not unbudgeted:
         out["token_variant"] = token_cost_run(w, prompts, sched, lens, n_steps, args.warmup, args.steps)
         out["token_variant"]["slowdown_vs_stop_head"] = value / out["token_variant"]["value"]
         out["token_variant"]["bytes_ratio_vs_stop_head"] = out["token_variant"]["algorithmic_bytes_per_run"] / alg_bytes

@@ -1,9 +1,11 @@
 // Weight GEMMs of the decode loop: C[m][n] = sum_k X[m][k] * W[n][k].
 //
 // Weights are stored fragment-tiled (device_common.h): every wave load of a
-// weight fragment is one contiguous 1 KB block.  Two matrix-core kernels share
-// one set of fused epilogues:
-//  * k_gemm_skinny (M <= 64 rows: decode, micro steps, LM head).  HBM-bound
+// weight fragment is one contiguous 1 KB block, and the waves of a workgroup
+// take interleaved k-fragments so that together they read one contiguous
+// window.  Four matrix-core kernels share one set of fused epilogues:
+//  * k_gemm_skinny (M <= 8 rows: decode, micro steps, LM head; up to 64 for
+//    the embedder's output epilogues).  HBM-bound
 //    weight streaming with non-temporal loads; four waves split the k-range of
 //    a 16*TN-column tile, and loads of the next batch of fragments are issued
 //    before the matrix instructions of the current one.  The k dimension may
@@ -12,8 +14,14 @@
 //    cross-workgroup synchronisation inside a kernel: on this GPU the L2 of one
 //    XCD is not coherent with the others, and the write-back fences that a
 //    handshake needs cost far more than a kernel boundary).
-//  * k_gemm_big (M > 64: prefill chunks, batched micro context rows): 128x128
-//    LDS-staged tiles, double buffered, 2x2 waves of 64x64.
+//  * k_gemm_staged (M <= 8): the skinny GEMM with eight waves whose X operand
+//    is built in LDS by a prologue (an RMSNorm of the residual plus pending
+//    partials, or the merge of the attention splits), so the kernel that
+//    would produce X disappears from the launch sequence.
+//  * k_gemm_wide (8 < M <= 256: batched decode, micro context rows): eight
+//    waves own eight column tiles and share X chunks through LDS.
+//  * k_gemm_big (larger M: prefill chunks): 128x128 LDS-staged tiles, double
+//    buffered, 2x2 waves of 64x64.
 // X rows are the A operand (padded to 16), weight rows the B operand, so the
 // accumulator's columns are output features: lane l holds column l & 15 of a
 // 16-column tile for rows 4*(l >> 4) + i.

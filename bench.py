@@ -318,6 +318,9 @@ def main() -> int:
         e1.record(stream)
         if profile:
             ham.load_library().ham_profile(rt.handle, 1)
+        # the host's enqueue time is taken from an idle GPU: otherwise the loop
+        # would also wait for the prefill through the full launch queue
+        torch.cuda.synchronize()
         h0 = time.perf_counter()
         for st in range(1, n_steps + 1):
             rt.macro_step(sched[st])

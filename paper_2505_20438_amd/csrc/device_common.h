@@ -123,6 +123,14 @@ __device__ __forceinline__ u4 buf_u4_stream(BufRsrc r, uint32_t off) {
   return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
 }
 
+// Workgroup barrier for data exchanged through LDS: this wave's LDS accesses
+// complete, then s_barrier.  __syncthreads also waits for every vector memory
+// operation the wave still has in flight (its release fence must cover global
+// stores), prefetched weight blocks included; this one lets them stay in flight.
+// Only for exchanges through LDS: global memory written before it is not
+// ordered for the other waves.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // pack 8 floats (bf16) / 4 floats (fp32) into one lane fragment
 __device__ __forceinline__ u4 pack_frag_bf16(const float* v) {
   u4 r;

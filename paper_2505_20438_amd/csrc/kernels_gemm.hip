@@ -353,9 +353,12 @@ __device__ __forceinline__ void stage_norm_load(const GemmArgs& a, NormLoads& L,
   }
 }
 
+// The summed residual (and the context copy, and the k-range's sums of squares
+// when the k-range is split) leave the workgroup later, in stage_norm_publish:
+// a global store in flight makes every later wait for a load a wait for all of
+// them (stores and loads share one counter here), prefetched weights included.
 template <typename T>
-__device__ __forceinline__ void stage_norm(const GemmArgs& a, NormLoads& L, char* stg, float* aux, int k0, int Kr,
-                                           int split, bool tile0) {
+__device__ __forceinline__ void stage_norm(const GemmArgs& a, NormLoads& L, char* stg, float* aux, int k0, int Kr) {
   const XStage& s = a.xs;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int M = a.M, cpr = Kr / 4, nch = M * cpr;
@@ -375,22 +378,16 @@ __device__ __forceinline__ void stage_norm(const GemmArgs& a, NormLoads& L, char
         if (q < ns) v[j] += pv[j][q];
       const f4 x = v[j];
       sq[i] = (x[0] * x[0] + x[1] * x[1]) + (x[2] * x[2] + x[3] * x[3]);
-      if (tile0) {
-        const int m = i / cpr, k = k0 + (i % cpr) * 4;
-        *reinterpret_cast<f4*>(s.x_out + (size_t)m * s.ldx + k) = x;
-        if (s.ctx) *reinterpret_cast<f4*>(s.ctx + (size_t)m * s.ldctx + k) = x;
-      }
     }
   }
-  __syncthreads();
+  lds_barrier();
   if (w < M) {  // wave m: the sum of squares of row m over this k-range, fixed order
     float t = 0.f;
     for (int c = lane; c < cpr; c += 64) t += sq[w * cpr + c];
     t = wave_sum(t);
     if (lane == 0) ssr[w] = t;
   }
-  __syncthreads();
-  if (!whole && tile0 && tid < M) s.ss_out[(size_t)split * M + tid] = ssr[tid];
+  lds_barrier();
 #pragma unroll
   for (int j = 0; j < STG_CH; ++j) {
     const int i = tid + j * STG_THREADS;
@@ -400,6 +397,25 @@ __device__ __forceinline__ void stage_norm(const GemmArgs& a, NormLoads& L, char
       stage_put4<T>(stg, Kr, m, kl, v[j] * sc * gv[j]);
     }
   }
+}
+
+// Column tile 0's workgroup of each k-range writes the summed residual rows (and
+// the context copy) and, when the k-range is split, the range's sums of squares.
+__device__ __forceinline__ void stage_norm_publish(const GemmArgs& a, const NormLoads& L, const float* aux, int k0,
+                                                   int Kr, int split) {
+  const XStage& s = a.xs;
+  const int tid = threadIdx.x;
+  const int M = a.M, cpr = Kr / 4, nch = M * cpr;
+#pragma unroll
+  for (int j = 0; j < STG_CH; ++j) {
+    const int i = tid + j * STG_THREADS;
+    if (i < nch) {
+      const int m = i / cpr, k = k0 + (i % cpr) * 4;
+      *reinterpret_cast<f4*>(s.x_out + (size_t)m * s.ldx + k) = L.v[j];
+      if (s.ctx) *reinterpret_cast<f4*>(s.ctx + (size_t)m * s.ldctx + k) = L.v[j];
+    }
+  }
+  if (gridDim.y > 1 && tid < M) s.ss_out[(size_t)split * M + tid] = aux[nch + tid];
 }
 
 // XS_ATTN prologue.  Heads h0.. of the k-range; one wave per (row, head)
@@ -471,7 +487,7 @@ __device__ __forceinline__ void stage_attn(const GemmArgs& a, AttnLoads& L, char
     const float L = wave_sum(e * ls);
     if (lane < ans) wts[gi * ans + lane] = L > 0.f ? e / L : 0.f;
   }
-  __syncthreads();
+  lds_barrier();
   if (act) {
     const float* wt = wts + (m * nh + (h - h0)) * ans;
     f4 acc = f4{0.f, 0.f, 0.f, 0.f};
@@ -482,7 +498,7 @@ __device__ __forceinline__ void stage_attn(const GemmArgs& a, AttnLoads& L, char
     }
     ps[tid] = acc;
   }
-  __syncthreads();
+  lds_barrier();
   for (int i = tid; i < nch; i += STG_THREADS) {
     f4 x = ps[i];
     for (int q = 1; q < SG; ++q) x += ps[q * nch + i];
@@ -549,9 +565,9 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
                                              : BUF_OOB);
   }
   __builtin_amdgcn_sched_barrier(0);
-  if constexpr (XS == XS_NORM) stage_norm<T>(a, pl, stg, aux, c0 * KB, Kr, split, ntile == 0);
+  if constexpr (XS == XS_NORM) stage_norm<T>(a, pl, stg, aux, c0 * KB, Kr);
   else stage_attn<T>(a, pl, stg, aux, c0 * KB, Kr);
-  __syncthreads();
+  lds_barrier();
   const int i0 = npf;
   const int nb = (cnt - i0) / U;
   u4 wc[U][TN], wn[U][TN];
@@ -608,6 +624,8 @@ __global__ __launch_bounds__(STG_THREADS) void k_gemm_staged(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) mma_act<T>(acc[0][j], h, l, bw[j]);
   }
+  if constexpr (XS == XS_NORM)
+    if (ntile == 0) stage_norm_publish(a, pl, aux, c0 * KB, Kr, split);
   skinny_finish<T, 1, TN, EPI, STG_NW>(a, acc, red, ntile, split, nsplit, n0);
 }
 

@@ -529,10 +529,14 @@ int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, con
   d.dbg_logits = m->dbg ? m->dbg + (size_t)k * y.B * y.V : nullptr;
   d.dbg_stop = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + (size_t)4 * y.B * y.d + (size_t)k * y.B : nullptr;
   d.stop_buf = m->WS<float>(y.stopb); d.best_val = m->WS<float>(y.bval); d.best_idx = m->WS<int>(y.bidx);
+  // the next micro step's input rows, written by the same launch (the micro
+  // decoder's rows start in the first residual buffer)
+  d.prep_k = k + 1 < y.G ? k + 1 : 0; d.C = y.C; d.d = y.d;
+  d.ctx = m->WS<float>(y.ctx); d.E = m->W<char>(y.E); d.x = m->WS<float>(y.x);
   int ns = 1;
   if (gemm_p(m, EPI_ARGMAX, ga, 1, k == 0 ? HAM_PROF_HEAD0 : HAM_PROF_HEADK, &ns))
     return fail(HAM_EINVAL, "lm head shape");
-  launch_decide(d, skinny_tiles(y.Vpad), B, m->s);
+  if (launch_decide(dtype_of(m), d, skinny_tiles(y.Vpad), B, m->s)) return fail(HAM_EINVAL, "decision shape");
   return HAM_OK;
 }
 
@@ -545,11 +549,7 @@ int decode_tail(ham_model* m, Pending& pend, float* ctx_last, float* xres, int* 
   if (rc) return rc;
   const long long lsb = (long long)y.Hk * LOCAL_SLOTS * y.hd, lsh = (long long)LOCAL_SLOTS * y.hd;
   for (int k = 1; k < y.G; ++k) {
-    MicroPrepArgs mp{};
-    mp.st = m->sp; mp.B = B; mp.C = y.C; mp.k = k; mp.d = y.d; mp.ctx = m->WS<float>(y.ctx);
-    mp.E = m->W<char>(y.E); mp.x = m->WS<float>(y.x);
-    launch_micro_prep(dt, mp, m->s);
-    float* x = m->WS<float>(y.x);  // micro-decoder rows start in the first residual buffer
+    float* x = m->WS<float>(y.x);  // written by decision k - 1
     RowMap rm{};
     rm.mode = k == 1 ? ROWS_MICRO1 : ROWS_MICROK; rm.C = y.C; rm.k = k; rm.st = m->sp;
     const int R = k == 1 ? B * (y.C + 1) : B;

@@ -84,6 +84,12 @@ struct DecideArgs {
   float* stop_buf;   // [B] stop logits (workspace)
   float* best_val;   // [n_wg][B] argmax partials
   int* best_idx;
+  // inputs of micro step prep_k (0: none) for the sequences still running:
+  // step 1 = [ctx_1..ctx_C, E[t_0]] per sequence, step k = E[t_{k-1}]
+  int prep_k, C, d;
+  const float* ctx;  // [B][C][d]
+  const void* E;     // embedding table
+  float* x;          // [rows][d]
 };
 
 // Where the skinny GEMM takes its X operand from.  XS_ACT: activation rows in
@@ -164,7 +170,7 @@ int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, 
 constexpr int GEMM_NO_STAGE = -2;
 // whether launch_gemm would take the staged path for these arguments (nothing launched)
 bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split);
-int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s);
+int launch_decide(int dtype, const DecideArgs& d, int ntiles, int M, Stream s);
 int skinny_tiles(int N);  // column tiles (argmax partials per row) of a skinny launch over N columns
 int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s);
 int launch_attn_decode(int dtype, const AttnArgs& a, Stream s);

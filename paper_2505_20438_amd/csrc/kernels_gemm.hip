@@ -739,15 +739,19 @@ __global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
 }
 
 // Final argmax of one row over all column tiles (fixed total order: larger value,
-// then lower index), then the decision and stop test of that sequence.  Each
-// thread issues all of its tile loads before comparing any of them.
+// then lower index), then the decision and stop test of that sequence, then
+// (a sequence still running) the input rows of the next micro step, so no
+// separate launch prepares them.  Each thread issues all of its tile loads
+// before comparing any of them.
 constexpr int DECIDE_THREADS = 1024;
 constexpr int DECIDE_PER = 8;  // tiles per thread: ntiles <= 8192
 
+template <typename T>
 __global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int ntiles, int M) {
   if (!any_flag(d.st.active, d.B)) return;
   __shared__ float sv[DECIDE_THREADS / 64];
   __shared__ int si[DECIDE_THREADS / 64];
+  __shared__ int s_run, s_tok;
   const int m = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   float v[DECIDE_PER];
@@ -782,6 +786,37 @@ __global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int nti
     for (int q = 1; q < DECIDE_THREADS / 64; ++q)
       if (better(sv[q], si[q], bv, bi)) { bv = sv[q]; bi = si[q]; }
     decide_one(d, m, bi, d.stop_buf[m]);
+    s_run = d.st.active[m];                    // this thread's own writes
+    s_tok = s_run ? d.st.grp_tok[m * 4 + d.prep_k - 1] : 0;
+  }
+  __syncthreads();
+  if (d.prep_k == 0 || !s_run) return;
+  // rows [ctx_1..ctx_C, E[t]] (step 1) or [E[t]]: 4-value chunks, every load of
+  // a batch in flight before its stores
+  const T* E = (const T*)d.E + (size_t)s_tok * d.d;
+  const int nc = d.prep_k == 1 ? d.C : 0;
+  const float* ctx = d.ctx + (size_t)m * d.C * d.d;
+  float* x = d.x + (size_t)m * (nc + 1) * d.d;
+  const int cpr = d.d / 4, total = (nc + 1) * cpr;
+  constexpr int PB = 4;
+  for (int i0 = threadIdx.x; i0 < total; i0 += PB * DECIDE_THREADS) {
+    f4 v[PB];
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const int i = i0 + u * DECIDE_THREADS;
+      if (i < nc * cpr) {
+        v[u] = *reinterpret_cast<const f4*>(ctx + (size_t)i * 4);
+      } else if (i < total) {
+        const int c = (i - nc * cpr) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[u][e] = to_f<T>(E[c + e]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const int i = i0 + u * DECIDE_THREADS;
+      if (i < total) *reinterpret_cast<f4*>(x + (size_t)i * 4) = v[u];
+    }
   }
 }
 
@@ -1119,10 +1154,12 @@ bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split) {
   return rc == 0;
 }
 
-int launch_decide(const DecideArgs& d, int ntiles, int M, Stream s) {
+int launch_decide(int dtype, const DecideArgs& d, int ntiles, int M, Stream s) {
   // ntiles: argmax partials written per row by the LM-head launch
   if (ntiles > DECIDE_THREADS * DECIDE_PER) return -1;
-  launch_k(k_decide, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles, M);
+  if (d.prep_k < 0 || d.prep_k > 3) return -1;
+  if (dtype == 1) launch_k(k_decide<bf16>, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles, M);
+  else launch_k(k_decide<float>, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles, M);
   return 0;
 }
 

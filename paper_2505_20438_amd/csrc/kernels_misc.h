@@ -39,14 +39,6 @@ struct GatherArgs {
   int* err;                         // set (bit 2) if an id is out of range
 };
 
-struct MicroPrepArgs {
-  SeqPtrs st;
-  int B, C, k, d;
-  const float* ctx;                 // [B][C][d]
-  const void* E;
-  float* x;                         // [rows][d]
-};
-
 struct GenArgs {
   void* dst; int rows, cols; long long row_off; int interleave; int tiled; uint64_t key;
 };
@@ -56,7 +48,6 @@ void launch_embed_attn(int dtype, const EmbedAttnArgs& a, Stream s);
 void launch_prefill_begin(const PrefillArgs& a, Stream s);
 void launch_gather_rows(int dtype, const GatherArgs& a, Stream s);
 void launch_copy_row(const float* src, float* dst, int d, Stream s);
-void launch_micro_prep(int dtype, const MicroPrepArgs& a, Stream s);
 void launch_gen_normal(int dtype, const GenArgs& a, Stream s);
 void launch_fill_f32(float* p, long long n, float v, Stream s);
 

@@ -403,24 +403,6 @@ __global__ __launch_bounds__(256) void k_copy_row(const float* src, float* dst, 
   for (int i = threadIdx.x; i < d; i += 256) dst[i] = src[i];
 }
 
-// micro-decoder inputs: step 1 = [ctx_1..ctx_C, E[t_0]] per sequence, step k = E[t_{k-1}]
-template <typename T>
-__global__ __launch_bounds__(256) void k_micro_prep(MicroPrepArgs a) {
-  const int r = blockIdx.x;
-  const int per = a.k == 1 ? a.C + 1 : 1;
-  const int b = r / per, c = r % per;
-  if (!a.st.active[b]) return;
-  float* x = a.x + (size_t)r * a.d;
-  const T* E = (const T*)a.E;
-  if (a.k == 1 && c < a.C) {
-    const float* src = a.ctx + ((size_t)b * a.C + c) * a.d;
-    for (int i = threadIdx.x; i < a.d; i += 256) x[i] = src[i];
-  } else {
-    const int t = a.st.grp_tok[b * 4 + a.k - 1];
-    for (int i = threadIdx.x; i < a.d; i += 256) x[i] = to_f<T>(E[(size_t)t * a.d + i]);
-  }
-}
-
 // ---------------------------------------------------------------- weight generator
 // SplitMix64 (Steele, Lea, Flood 2014): i-th output of the stream seeded with s.
 __device__ __forceinline__ uint64_t sm64(uint64_t s, uint64_t i) {
@@ -477,10 +459,6 @@ void launch_gather_rows(int dtype, const GatherArgs& a, Stream s) {
 }
 void launch_copy_row(const float* src, float* dst, int d, Stream s) {
   launch_k(k_copy_row, dim3(1), dim3(256), 0, s, src, dst, d);
-}
-void launch_micro_prep(int dtype, const MicroPrepArgs& a, Stream s) {
-  const int rows = a.k == 1 ? a.B * (a.C + 1) : a.B;
-  HAM_T_LAUNCH(dtype, k_micro_prep, dim3(rows), dim3(256), s, a);
 }
 void launch_gen_normal(int dtype, const GenArgs& a, Stream s) {
   const long long count = (long long)a.rows * a.cols;

@@ -319,18 +319,32 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
   const int grp = a.H / a.Hkv;
   const T* Kb = (const T*)a.K + (size_t)r * a.sb + kvh * a.sh;  // decode rows: row r is sequence r
   const T* Vb = (const T*)a.VT + (size_t)r * a.sb + kvh * a.sh;
-  // this wave's key blocks: static share of the split's blocks of [0, kv_cap)
-  const int nblk_all = (a.kv_cap + KB - 1) / KB;
-  const int per = (nblk_all + a.nsplit - 1) / a.nsplit;
-  const int sb0 = min(nblk_all, split * per), sb1 = min(nblk_all, sb0 + per);
-  const int b0 = sb0 + w * (sb1 - sb0) / ATTN_NW, b1 = sb0 + (w + 1) * (sb1 - sb0) / ATTN_NW;
+  // this wave's key blocks.  Split launches: a static share of the split's
+  // blocks of [0, kv_cap), so the first loads need nothing from memory.  One
+  // workgroup per row: an even share of the row's own cached blocks (rows
+  // shorter than kv_cap would leave the last waves idle while the first ones
+  // carry a full share), at the cost of reading the row's length first.
+  int b0, b1;
+  RowInfo ri;
+  if (a.nsplit == 1) {
+    ri = row_info(a.rm, r);
+    const int nb = (min(max(ri.n_valid - 1, 0), a.kv_cap) + KB - 1) / KB;
+    b0 = w * nb / ATTN_NW;
+    b1 = (w + 1) * nb / ATTN_NW;
+  } else {
+    const int nblk_all = (a.kv_cap + KB - 1) / KB;
+    const int per = (nblk_all + a.nsplit - 1) / a.nsplit;
+    const int sb0 = min(nblk_all, split * per), sb1 = min(nblk_all, sb0 + per);
+    b0 = sb0 + w * (sb1 - sb0) / ATTN_NW;
+    b1 = sb0 + (w + 1) * (sb1 - sb0) / ATTN_NW;
+  }
   // first chunk of keys in flight before anything else
   KVBlock<T, HD> blk[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i)
     if (b0 + i < b1) kv_load<T, HD>(blk[i], Kb, Vb, a.S, (b0 + i) * KB);
   if (!any_flag(a.gate, a.gate_n)) return;
-  const RowInfo ri = row_info(a.rm, r);
+  if (a.nsplit != 1) ri = row_info(a.rm, r);
   // the projection values of this kv head: one 4-float chunk per thread, all splits
   const int nch = (grp + 2) * HD / 4;
   const int ns = a.part ? a.nsplit_qkv : 1;

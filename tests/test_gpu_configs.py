@@ -122,6 +122,19 @@ def test_batch20_ragged_8b_dims_teacher_forced(torch_cuda):
     assert ties <= max(1, exact // 50)
 
 
+def test_batch32_one_workgroup_per_row_attention(torch_cuda):
+    # 32 rows x 8 KV heads fill the GPU with one attention workgroup per (row, head):
+    # the waves split each row's own cached blocks (rows of different lengths)
+    shp = dataclasses.replace(SHAPE_8B, n_layers=2, micro_layers=1, vocab=8192)
+    B, P, steps = 32, 100, 4
+    prompts = synth.prompt_ids(4005, B, P, shp.vocab)
+    sched = synth.group_schedule(5005, B, steps + 1, 4)
+    budgets = [0, 2, 5, 9] * 8
+    om = OracleHam(shp, 6005, cache_f64=True)
+    exact, ties = _teacher_forced(om, shp, prompts, budgets, steps, sched, 6005, debug_steps=steps + 1)
+    assert ties <= max(1, exact // 50)
+
+
 def _expected_lengths(sched_row, budget):
     out, emitted, s = [], 0, 0
     while emitted < budget:

@@ -529,6 +529,7 @@ int run_decision(ham_model* m, int k, float* x, int row_stride, int row_off, con
   d.dbg_logits = m->dbg ? m->dbg + (size_t)k * y.B * y.V : nullptr;
   d.dbg_stop = m->dbg ? m->dbg + (size_t)4 * y.B * y.V + (size_t)4 * y.B * y.d + (size_t)k * y.B : nullptr;
   d.stop_buf = m->WS<float>(y.stopb); d.best_val = m->WS<float>(y.bval); d.best_idx = m->WS<int>(y.bidx);
+  d.ntiles = skinny_tiles(y.Vpad);
   // the next micro step's input rows, written by the same launch (the micro
   // decoder's rows start in the first residual buffer)
   d.prep_k = k + 1 < y.G ? k + 1 : 0; d.C = y.C; d.d = y.d;

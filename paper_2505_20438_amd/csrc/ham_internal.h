@@ -82,8 +82,9 @@ struct DecideArgs {
   float* dbg_logits; // [B][V] for this k, or null
   float* dbg_stop;   // [B] for this k, or null
   float* stop_buf;   // [B] stop logits (workspace)
-  float* best_val;   // [n_wg][B] argmax partials
+  float* best_val;   // [B][ntiles] argmax partials per column tile (a row's are contiguous)
   int* best_idx;
+  int ntiles;
   // inputs of micro step prep_k (0: none) for the sequences still running:
   // step 1 = [ctx_1..ctx_C, E[t_0]] per sequence, step k = E[t_{k-1}]
   int prep_k, C, d;

@@ -270,8 +270,8 @@ __device__ __forceinline__ void skinny_epilogue(const GemmArgs& a, f4 (*acc)[TN]
           if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
         }
         if (r16 == 0 && m < a.M) {
-          d.best_val[(size_t)ntile * a.M + m] = bv;
-          d.best_idx[(size_t)ntile * a.M + m] = bi;
+          d.best_val[(size_t)m * d.ntiles + ntile] = bv;
+          d.best_idx[(size_t)m * d.ntiles + ntile] = bi;
         }
       }
   } else {
@@ -747,7 +747,7 @@ constexpr int DECIDE_THREADS = 1024;
 constexpr int DECIDE_PER = 8;  // tiles per thread: ntiles <= 8192
 
 template <typename T>
-__global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int ntiles, int M) {
+__global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int ntiles) {
   if (!any_flag(d.st.active, d.B)) return;
   __shared__ float sv[DECIDE_THREADS / 64];
   __shared__ int si[DECIDE_THREADS / 64];
@@ -762,8 +762,8 @@ __global__ __launch_bounds__(DECIDE_THREADS) void k_decide(DecideArgs d, int nti
     v[q] = -INFINITY;
     ix[q] = 0x7fffffff;
     if (t < ntiles) {
-      v[q] = d.best_val[(size_t)t * M + m];
-      ix[q] = d.best_idx[(size_t)t * M + m];
+      v[q] = d.best_val[(size_t)m * ntiles + t];
+      ix[q] = d.best_idx[(size_t)m * ntiles + t];
     }
   }
   float bv = -INFINITY;
@@ -1156,10 +1156,10 @@ bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split) {
 
 int launch_decide(int dtype, const DecideArgs& d, int ntiles, int M, Stream s) {
   // ntiles: argmax partials written per row by the LM-head launch
-  if (ntiles > DECIDE_THREADS * DECIDE_PER) return -1;
+  if (ntiles > DECIDE_THREADS * DECIDE_PER || ntiles != d.ntiles) return -1;
   if (d.prep_k < 0 || d.prep_k > 3) return -1;
-  if (dtype == 1) launch_k(k_decide<bf16>, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles, M);
-  else launch_k(k_decide<float>, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles, M);
+  if (dtype == 1) launch_k(k_decide<bf16>, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles);
+  else launch_k(k_decide<float>, dim3(M), dim3(DECIDE_THREADS), 0, s, d, ntiles);
   return 0;
 }
 

@@ -544,13 +544,14 @@ __global__ __launch_bounds__(COMBINE_THREADS) void k_attn_combine(AttnArgs a) {
 
 // Prefill: causal attention of a prompt chunk (rows of mode PREFILL: slots
 // t0 + r of one sequence).  One workgroup of PF_NW waves per (row chunk, kv
-// head): wave w takes q-head kvh*grp + w % grp and the 16 rows 16*(w / grp)..
-// of the chunk, so a chunk is 16*(PF_NW / grp) rows.  The key blocks pass
-// through LDS once per workgroup, PF_NBL blocks per stage, double-buffered:
-// the global loads are contiguous, and each 16-byte piece is stored where a
-// wave's operand fragment expects it (K as [tile][fragment][lane], V^T as
-// [d-tile][lane]), so every operand read of a wave is one contiguous 1 KB.
-constexpr int PF_NW = 8, PF_NBL = 2;
+// head): wave w takes q-head kvh*grp + w % grp and PF_RT tiles of 16 rows from
+// row 16*PF_RT*(w / grp) of the chunk, so a chunk is 16*PF_RT*(PF_NW / grp)
+// rows; each key block a wave reads from LDS serves all its row tiles.  The key
+// blocks pass through LDS once per workgroup, PF_NBL blocks per stage,
+// double-buffered: the global loads are contiguous, and each 16-byte piece is
+// stored where a wave's operand fragment expects it (K as [tile][fragment][lane],
+// V^T as [d-tile][lane]), so every operand read of a wave is one contiguous 1 KB.
+constexpr int PF_NW = 8, PF_NBL = 2, PF_RT = 2;
 template <typename T, int HD>
 struct PrefillBlock {  // 16-byte pieces of one key block: K, then V
   static constexpr int KB = Frag<T>::KB, EPL = Frag<T>::EPL, NF = HD / KB, ND = HD / 16, TT = KB / 16;
@@ -566,31 +567,36 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
   __shared__ u4 lds[2][SU];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int kvh = blockIdx.y;
-  const int grp = a.H / a.Hkv, nrg = PF_NW / grp, RB = 16 * nrg;
+  const int grp = a.H / a.Hkv, nrg = PF_NW / grp, RB = 16 * PF_RT * nrg;
   const int jh = w % grp, rg = w / grp;
   const int h = kvh * grp + jh;
   const int chunk0 = blockIdx.x * RB;
   if (chunk0 >= a.R) return;  // the same for every wave of the workgroup
   const RowInfo r0 = row_info(a.rm, chunk0);
   const int wg_end = r0.slot + min(RB, a.R - chunk0);  // keys [0, wg_end)
-  const int row0 = chunk0 + rg * 16;
+  const int row0 = chunk0 + rg * 16 * PF_RT;
   const bool rows_ok = rg < nrg && row0 < a.R;          // waves past the q-heads only load
-  const int wave_end = rows_ok ? r0.slot + (row0 - chunk0) + min(16, a.R - row0) : 0;
+  const int wave_end = rows_ok ? r0.slot + (row0 - chunk0) + min(16 * PF_RT, a.R - row0) : 0;
   const T* Kb = (const T*)a.K + r0.b * a.sb + kvh * a.sh;
   const T* Vb = (const T*)a.VT + r0.b * a.sb + kvh * a.sh;
 
-  const int qrow = row0 + r16;
-  const bool qok = rows_ok && qrow < a.R;
-  u4 qf[NF], ql[NF];
+  u4 qf[PF_RT][NF], ql[PF_RT][NF];
+  int limit[PF_RT], tile_end[PF_RT];
   constexpr int PL = Act<T>::PL;
-  const T* qp = (const T*)a.q + (size_t)(qok ? qrow : 0) * a.ldq * PL + (size_t)h * HD + g * EPL;
 #pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    qf[f] = qok ? ld16(qp + f * KB) : zero16();
-    ql[f] = (Act<T>::SPLIT && qok) ? ld16(qp + a.ldq + f * KB) : zero16();
+  for (int t = 0; t < PF_RT; ++t) {
+    const int trow = row0 + 16 * t, qrow = trow + r16;
+    const bool qok = rows_ok && qrow < a.R;
+    const T* qp = (const T*)a.q + (size_t)(qok ? qrow : 0) * a.ldq * PL + (size_t)h * HD + g * EPL;
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      qf[t][f] = qok ? ld16(qp + f * KB) : zero16();
+      ql[t][f] = (Act<T>::SPLIT && qok) ? ld16(qp + a.ldq + f * KB) : zero16();
+    }
+    // causal: the row at slot s sees slots [0, s]
+    limit[t] = qok ? r0.slot + (qrow - chunk0) + 1 : 0;
+    tile_end[t] = (rows_ok && trow < a.R) ? r0.slot + (trow - chunk0) + min(16, a.R - trow) : 0;
   }
-  // causal: the row at slot s sees slots [0, s]
-  const int limit = qok ? r0.slot + (qrow - chunk0) + 1 : 0;
 
   const int nblk = (wg_end + KB - 1) / KB, nst = (nblk + PF_NBL - 1) / PF_NBL;
   // piece c of a key block: global source and LDS position
@@ -632,10 +638,15 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
     }
   };
 
-  f4 o[ND];
+  f4 o[PF_RT][ND];
+  float mrun[PF_RT], lrun[PF_RT];
 #pragma unroll
-  for (int dt = 0; dt < ND; ++dt) o[dt] = f4{0.f, 0.f, 0.f, 0.f};
-  float mrun = -INFINITY, lrun = 0.f;
+  for (int t = 0; t < PF_RT; ++t) {
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) o[t][dt] = f4{0.f, 0.f, 0.f, 0.f};
+    mrun[t] = -INFINITY;
+    lrun[t] = 0.f;
+  }
   const float scale = 1.0f / sqrtf((float)HD);
   if (nst > 0) {
     gload(0);
@@ -657,7 +668,10 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
           for (int f = 0; f < NF; ++f) kv.k[t][f] = bp[(t * NF + f) * 64 + lane];
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) kv.v[dt] = bp[KU + dt * 64 + lane];
-        attn_block<T, HD>(kv, blk * KB, limit, wave_end, qf, ql, scale, mrun, lrun, o);
+#pragma unroll
+        for (int t = 0; t < PF_RT; ++t)
+          if (blk * KB < tile_end[t])
+            attn_block<T, HD>(kv, blk * KB, limit[t], wave_end, qf[t], ql[t], scale, mrun[t], lrun[t], o[t]);
       }
     }
     if (st + 1 < nst) lstore(st + 1, buf ^ 1);  // the other buffer was last read before the previous barrier
@@ -665,15 +679,18 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
   }
   if (!rows_ok) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int jr = 4 * g + i;  // query row within the wave
-    const float lj = __shfl(lrun, jr, WAVE);
-    if (row0 + jr < a.R) {
-      const float inv = lj > 0.f ? 1.0f / lj : 0.f;
+  for (int t = 0; t < PF_RT; ++t)
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, row0 + jr, a.ldo, h * HD + r16 + dt * 16, o[dt][i] * inv);
+    for (int i = 0; i < 4; ++i) {
+      const int jr = 4 * g + i;  // query row within the tile
+      const float lj = __shfl(lrun[t], jr, WAVE);
+      const int row = row0 + 16 * t + jr;
+      if (row < a.R) {
+        const float inv = lj > 0.f ? 1.0f / lj : 0.f;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) Act<T>::put(a.o, row, a.ldo, h * HD + r16 + dt * 16, o[t][dt][i] * inv);
+      }
     }
-  }
 }
 
 template <typename T>
@@ -689,7 +706,7 @@ template <typename T>
 static int prefill_t(const AttnArgs& a, Stream s) {
   const int grp = a.H / a.Hkv;
   if (grp < 1 || grp > PF_NW) return -1;
-  const int rb = 16 * (PF_NW / grp);  // rows per workgroup
+  const int rb = 16 * PF_RT * (PF_NW / grp);  // rows per workgroup
   dim3 grid((a.R + rb - 1) / rb, a.Hkv);
   if (a.hd == 64) launch_k((k_attn_prefill<T, 64>), grid, dim3(64 * PF_NW), 0, s, a);
   else if (a.hd == 128) launch_k((k_attn_prefill<T, 128>), grid, dim3(64 * PF_NW), 0, s, a);

@@ -155,6 +155,18 @@ def test_small_fp32_teacher_forced_ragged_batch(torch_cuda):
     assert ties == 0
 
 
+def test_small_fp32_long_prompt_teacher_forced(torch_cuda):
+    # prompt chunks above 256 rows: the prefill runs the 128x128-tile GEMM and
+    # several 64-row attention chunks, in fp32 (no rounding to hide behind)
+    shp = dataclasses.replace(SMALL16, dtype=0)
+    B, P, steps = 2, 300, 6
+    prompts = synth.prompt_ids(79, B, P, shp.vocab)
+    sched = synth.group_schedule(80, B, steps + 1, 4)
+    om = OracleHam(shp, 81)
+    exact, ties = _teacher_forced(om, shp, prompts, [0, 9], steps, sched, 81, debug_steps=steps + 1)
+    assert ties == 0
+
+
 def test_1b_bf16_teacher_forced_prefix(torch_cuda):
     # configuration 2 shape and prompt length; the first macro-steps against the oracle
     w = WORKLOADS["c2_1b_bf16"]

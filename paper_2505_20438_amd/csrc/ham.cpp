@@ -851,16 +851,19 @@ int macro_step_body(ham_model* m, int32_t* d_out_tokens, int32_t* d_out_lens) {
   ea.part = ns > 1 ? m->WS<float>(y.part) : nullptr; ea.nsplit = ns;
   ea.out = m->WS<char>(y.emb_o);
   launch_embed_attn(dt, ea, s);
+  // the embedder's two output projections run unsplit: a split would need a
+  // reduce launch, which costs about as much as the slower GEMM even when no
+  // group is fused and the whole chain is gated off
   ga.W = m->W<char>(y.Ao); ga.N = y.d; ga.K = y.HD; ga.X = m->WS<char>(y.emb_o); ga.ldx = y.HD; ga.M = B;
   ga.out = m->WS<char>(y.emb_y); ga.ldo = y.d;
-  if (gemm_p(m, EPI_OP, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
+  if (gemm_p(m, EPI_OP, ga, 1, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
   if (ns > 1) {
     ga.nsplit = ns;
     if (launch_split_reduce(dt, EPI_OP, ga, s)) return fail(HAM_EINVAL, "split reduce shape");
   }
   ga.W = m->W<char>(y.Alin); ga.N = y.d; ga.K = y.d; ga.X = m->WS<char>(y.emb_y); ga.ldx = y.d;
   ga.out = x; ga.ldo = y.d; ga.rowmask = m->sp.fused;
-  if (gemm_p(m, EPI_XMASK, ga, MAX_GEMM_SPLIT, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
+  if (gemm_p(m, EPI_XMASK, ga, 1, HAM_PROF_EMBED, &ns)) return fail(HAM_EINVAL, "embedder gemm shape");
   if (ns > 1) {
     ga.nsplit = ns;
     if (launch_split_reduce(dt, EPI_XMASK, ga, s)) return fail(HAM_EINVAL, "split reduce shape");

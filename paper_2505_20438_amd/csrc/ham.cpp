@@ -877,7 +877,10 @@ int macro_step_body(ham_model* m, int32_t* d_out_tokens, int32_t* d_out_lens) {
   // can hold, so every macro-step launches the same kernels with the same
   // arguments (graph replay); each row attends over its own device-side length
   const int kv_cap = std::min(m->prompt_len + y.steps - 1, y.S - 1);
-  const int nsplit = attn_step_splits(dt, B, y.Hk, y.hd, kv_cap);
+  // at most 16 splits while the batch is small enough for the o-projection's
+  // prologue to merge them (more would need a separate combine launch)
+  const int nsplit = B <= 8 ? std::min(16, attn_step_splits(dt, B, y.Hk, y.hd, kv_cap))
+                            : attn_step_splits(dt, B, y.Hk, y.hd, kv_cap);
   const StepAttn bstep{m->WS<float>(y.rope_cs), m->WS<float>(y.rope_cs) + y.hd / 2, y.hd, kv_cap};
   float* ctx = m->WS<float>(y.ctx);
   Pending pend;

@@ -110,6 +110,18 @@ def test_8b_shapes_reduced_depth_teacher_forced(torch_cuda):
     assert ties <= 1
 
 
+def test_8b_dims_long_prompt_split_attention_teacher_forced(torch_cuda):
+    # head dim 128 with a prompt long enough for several decode-attention splits,
+    # merged in the o-projection's prologue
+    shp = dataclasses.replace(SHAPE_8B, n_layers=2, micro_layers=1, vocab=8192)
+    B, P, steps = 1, 560, 4
+    prompts = synth.prompt_ids(4006, B, P, shp.vocab)
+    sched = synth.group_schedule(5006, B, steps + 1, 4)
+    om = OracleHam(shp, 6006)
+    exact, ties = _teacher_forced(om, shp, prompts, [0], steps, sched, 6006, debug_steps=steps + 1)
+    assert ties <= 1
+
+
 def test_batch20_ragged_8b_dims_teacher_forced(torch_cuda):
     # batch above 16 rows (two row tiles) and micro context rows above 64 (LDS-tiled GEMM)
     shp = dataclasses.replace(SHAPE_8B, n_layers=2, micro_layers=1, vocab=8192)

@@ -312,6 +312,32 @@ int norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* g
   return launch_rmsnorm(dtype_of(m), na, m->s) ? fail(HAM_EINVAL, "rmsnorm shape") : HAM_OK;
 }
 
+// The RMSNorm feeding GEMM `ga` (rows x, gain g): where the batched GEMM can
+// build the normed operand itself (XS_NORMW), only the norm's first phase
+// launches; otherwise the whole norm writes the operand buffer (XS_ACT).
+int norm_into_gemm(ham_model* m, GemmArgs& ga, int epi, float* x, int R, const float* g, Pending& pend,
+                   float* ctx, int ldctx, const int* gate, int gate_n) {
+  const Layout& y = m->y;
+  GemmArgs gw = ga;
+  gw.xsrc = XS_NORMW;
+  gw.xs.x = x; gw.xs.ldx = y.d; gw.xs.g = g; gw.xs.eps = m->cfg.norm_eps;
+  gw.xs.ssw = m->WS<float>(y.nss); gw.xs.nchw = (y.d + 255) / 256;
+  if (gemm_stage_fits(dtype_of(m), epi, gw, MAX_GEMM_SPLIT)) {
+    NormArgs na{};
+    na.x = x; na.ldx = y.d; na.row_stride = 1; na.row_off = 0; na.g = g; na.d = y.d; na.R = R;
+    na.eps = m->cfg.norm_eps; na.part = pend.part; na.nsplit = pend.nsplit; na.pM = pend.M;
+    na.ctx = ctx; na.ldctx = ldctx; na.gate = gate; na.gate_n = gate_n; na.ss = m->WS<float>(y.nss);
+    if (launch_norm_reduce(na, m->s) == 0) {
+      pend = Pending{};
+      ga = gw;
+      return HAM_OK;
+    }
+  }
+  if (norm_rows(m, x, R, 1, 0, g, pend, ctx, ldctx, nullptr, gate, gate_n)) return HAM_EINVAL;
+  ga.xsrc = XS_ACT; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+  return HAM_OK;
+}
+
 // The rest of a layer after attention: o-projection into the residual, second
 // norm, gate/up with the SwiGLU epilogue, down-projection into the residual.
 template <typename GK>
@@ -326,12 +352,13 @@ int layer_tail(ham_model* m, int j, int R, float* x, int split, const int* gate,
   if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_O), &ns)) return fail(HAM_EINVAL, "o-proj gemm shape");
   if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
 
-  if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n)) return HAM_EINVAL;
-
-  ga.W = m->W<char>(y.Wgu[j]); ga.N = 2 * y.F; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+  ga.W = m->W<char>(y.Wgu[j]); ga.N = 2 * y.F; ga.K = y.d;
   ga.out = m->WS<char>(y.act); ga.ldo = y.F;
+  if (norm_into_gemm(m, ga, EPI_SWIGLU, x, R, m->W<float>(y.g2[j]), pend, nullptr, 0, gate, gate_n))
+    return HAM_EINVAL;
   if (gemm_p(m, EPI_SWIGLU, ga, 1, gk(HAM_PROF_GU), &ns)) return fail(HAM_EINVAL, "gate/up gemm shape");
 
+  ga.xsrc = XS_ACT;
   ga.W = m->W<char>(y.Wd[j]); ga.N = y.d; ga.K = y.F; ga.X = m->WS<char>(y.act); ga.ldx = y.F;
   ga.out = x; ga.ldo = y.d;
   if (gemm_p(m, EPI_RESID, ga, split, gk(HAM_PROF_DOWN), &ns)) return fail(HAM_EINVAL, "down gemm shape");
@@ -396,8 +423,9 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   const int qkv_split = std::min(split, attn_step_max_qkv_split());
   const bool q_staged = gemm_stage_fits(dt, EPI_F32, ga, qkv_split);
   if (!q_staged) {
-    if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n)) return HAM_EINVAL;
-    ga.xsrc = XS_ACT; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+    ga.xsrc = XS_ACT;
+    if (norm_into_gemm(m, ga, EPI_F32, x, R, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, gate, gate_n))
+      return HAM_EINVAL;
   }
   if (gemm_p(m, EPI_F32, ga, qkv_split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
   if (q_staged) {
@@ -445,8 +473,9 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   gu.xs.g = m->W<float>(y.g2[j]); gu.xs.eps = eps; gu.xs.x_out = other(x);
   const bool u_staged = gemm_stage_fits(dt, EPI_SWIGLU, gu, 1);
   if (!u_staged) {
-    if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g2[j]), pend, nullptr, 0, nullptr, gate, gate_n)) return HAM_EINVAL;
-    gu.xsrc = XS_ACT; gu.X = m->WS<char>(y.xn); gu.ldx = y.d;
+    gu.xsrc = XS_ACT;
+    if (norm_into_gemm(m, gu, EPI_SWIGLU, x, R, m->W<float>(y.g2[j]), pend, nullptr, 0, gate, gate_n))
+      return HAM_EINVAL;
   }
   if (gemm_p(m, EPI_SWIGLU, gu, 1, gk(HAM_PROF_GU), &ns)) return fail(HAM_EINVAL, "gate/up gemm shape");
   if (u_staged) {
@@ -483,12 +512,17 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool pref
                           kv_visible, *step, base);
   const int split = prefill ? 1 : MAX_GEMM_SPLIT;
   int ns = 1;
-  if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n)) return HAM_EINVAL;
-
   GemmArgs ga{};
   ga.part = m->WS<float>(y.part); ga.gate = gate; ga.gate_n = gate_n;
-  ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.X = m->WS<char>(y.xn); ga.ldx = y.d; ga.M = R;
+  ga.W = m->W<char>(y.Wqkv[j]); ga.N = y.QKV; ga.K = y.d; ga.M = R;
   ga.out = m->WS<float>(y.qkv); ga.ldo = y.QKV;
+  if (prefill) {
+    if (norm_rows(m, x, R, 1, 0, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, nullptr, gate, gate_n))
+      return HAM_EINVAL;
+    ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+  } else if (norm_into_gemm(m, ga, EPI_F32, x, R, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, gate, gate_n)) {
+    return HAM_EINVAL;
+  }
   if (gemm_p(m, EPI_F32, ga, split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
 
   RopeArgs ra{};

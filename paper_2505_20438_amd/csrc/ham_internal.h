@@ -105,7 +105,10 @@ struct DecideArgs {
 //    (never x itself: other workgroups are still reading it) and to ctx.
 //  XS_ATTN: X = attention output combined from the split records of the
 //    decode attention (log-sum-exp weights per head, splits in order).
-enum XSource { XS_ACT = 0, XS_NORM = 1, XS_ATTN = 2 };
+//  XS_NORMW (batched GEMM, 8 < M <= 256): X = g * x * rinv from fp32 rows x whose
+//    pending partials the norm's first phase has already folded in; rinv from
+//    that phase's 256-column chunk sums of squares ssw [M][nchw].
+enum XSource { XS_ACT = 0, XS_NORM = 1, XS_ATTN = 2, XS_NORMW = 3 };
 struct XStage {
   const float* x; int ldx;             // NORM: residual rows [M][ldx]
   const float* part; int nsplit, pM;   // NORM: pending partials [nsplit][pM][ldx], or null
@@ -116,6 +119,7 @@ struct XStage {
   const float* rec_o;                  // ATTN: unnormalised outputs [M][Hkv][ans][grp][hd]
   const float* rec_ml;                 // ATTN: (max, sum) [M][Hkv][ans][grp][2]
   int ans, Hkv, grp, hd;               // ATTN: splits, heads, head dim
+  const float* ssw; int nchw;          // NORMW: chunk sums of squares [M][nchw]
 };
 
 struct GemmArgs {
@@ -203,5 +207,7 @@ struct NormArgs {
   float* ss;                                          // scratch [R][d/256] for the two-phase form, or null
 };
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s);
+// the norm's first phase alone, for 16..256 rows feeding an XS_NORMW GEMM (-1: does not apply)
+int launch_norm_reduce(const NormArgs& a, Stream s);
 
 }  // namespace ham

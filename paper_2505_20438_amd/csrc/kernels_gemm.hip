@@ -640,7 +640,11 @@ constexpr int WIDE_NW = 8;
 constexpr int WIDE_KC = 128;
 constexpr int MAX_WIDE_SWIGLU_SPLIT = 4;
 
-template <typename T, int MT, int TN, int EPI, int TAG>
+// NX: X is the RMSNorm of fp32 rows whose sums of squares the norm's first
+// phase left in 256-column chunks (XS_NORMW): each staged chunk is scaled by
+// the row's 1/rms and the gain and split into the operand planes here, in the
+// order and precision the norm's second phase would use.
+template <typename T, int MT, int TN, int EPI, int TAG, bool NX = false>
 __global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int KC = MT <= 4 ? WIDE_KC : WIDE_KC / 2;  // k per chunk: LDS holds two chunks of all rows
@@ -668,28 +672,82 @@ __global__ __launch_bounds__(64 * WIDE_NW) void k_gemm_wide(GemmArgs a) {
   for (int j = 0; j < TN; ++j)  // a wave past the last tile streams the last tile's blocks (never used)
     wrow[j] = W + (size_t)((tile_ok ? ntile : ntiles - 1) * TN + j) * nfr * 64 * EPL + (size_t)lane * EPL;
 
-  u4 xr[IPT];
+  constexpr int Q4 = KC / 4;                                   // NX: 4-value pieces per row of a chunk
+  constexpr int IPTN = NX ? (RT * Q4 + 64 * WIDE_NW - 1) / (64 * WIDE_NW) : 1;
+  __shared__ float rinv_s[NX ? RT : 1];
+  u4 xr[NX ? 1 : IPT];
+  f4 xv[IPTN], xg[IPTN];
   auto xload = [&](int c) {
+    if constexpr (NX) {
 #pragma unroll
-    for (int q = 0; q < IPT; ++q) {
-      const int i = tid + q * 64 * WIDE_NW;
-      xr[q] = zero16();
-      if (i < ITEMS) {
-        const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
-        if (m < a.M) xr[q] = ld16(X + ((size_t)m * PL + p) * a.ldx + (size_t)c * KC + pc * (16 / (int)sizeof(T)));
+      for (int q = 0; q < IPTN; ++q) {
+        const int i = tid + q * 64 * WIDE_NW;
+        xv[q] = f4{0.f, 0.f, 0.f, 0.f};
+        xg[q] = f4{0.f, 0.f, 0.f, 0.f};
+        if (i < RT * Q4) {
+          const int m = i / Q4, col = c * KC + (i % Q4) * 4;
+          xg[q] = *reinterpret_cast<const f4*>(a.xs.g + col);
+          if (m < a.M) xv[q] = *reinterpret_cast<const f4*>(a.xs.x + (size_t)m * a.xs.ldx + col);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < IPT; ++q) {
+        const int i = tid + q * 64 * WIDE_NW;
+        xr[q] = zero16();
+        if (i < ITEMS) {
+          const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
+          if (m < a.M) xr[q] = ld16(X + ((size_t)m * PL + p) * a.ldx + (size_t)c * KC + pc * (16 / (int)sizeof(T)));
+        }
       }
     }
   };
   auto xstore = [&](int buf) {
+    if constexpr (NX) {
 #pragma unroll
-    for (int q = 0; q < IPT; ++q) {
-      const int i = tid + q * 64 * WIDE_NW;
-      if (i < ITEMS) {
-        const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
-        *reinterpret_cast<u4*>(&xs[buf][m][p][pc * 16]) = xr[q];
+      for (int q = 0; q < IPTN; ++q) {
+        const int i = tid + q * 64 * WIDE_NW;
+        if (i < RT * Q4) {
+          const int m = i / Q4, k4 = (i % Q4) * 4;
+          const float inv = rinv_s[m];
+          f4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = xv[q][e] * inv * xg[q][e];
+          if constexpr (Act<T>::SPLIT) {
+            uint32_t h[4], l[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const bf16 hb = f2bf(v[e]);
+              h[e] = hb;
+              l[e] = f2bf(v[e] - bf2f(hb));
+            }
+            *reinterpret_cast<uint2*>(&xs[buf][m][0][k4 * 2]) = uint2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+            *reinterpret_cast<uint2*>(&xs[buf][m][PL - 1][k4 * 2]) = uint2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
+          } else {
+            *reinterpret_cast<f4*>(&xs[buf][m][0][k4 * 4]) = v;
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < IPT; ++q) {
+        const int i = tid + q * 64 * WIDE_NW;
+        if (i < ITEMS) {
+          const int m = i / (PL * PIECES), p = (i / PIECES) % PL, pc = i % PIECES;
+          *reinterpret_cast<u4*>(&xs[buf][m][p][pc * 16]) = xr[q];
+        }
       }
     }
   };
+  if constexpr (NX) {  // each row's 1/rms from the chunk sums, summed in chunk order
+    for (int m = tid; m < RT; m += 64 * WIDE_NW) {
+      float t = 0.f;
+      if (m < a.M)
+        for (int c = 0; c < a.xs.nchw; ++c) t += a.xs.ssw[(size_t)m * a.xs.nchw + c];
+      rinv_s[m] = m < a.M ? 1.0f / sqrtf(t / (float)a.K + a.xs.eps) : 0.f;
+    }
+    __syncthreads();
+  }
   u4 wa[FPC][TN], wb[FPC][TN];
   auto wload = [&](u4 (*dst)[TN], int c) {
 #pragma unroll
@@ -1049,7 +1107,7 @@ static int gemm_staged(const GemmArgs& a0, int max_split, int tag, Stream s, int
 
 // Batched rows: X through LDS once per workgroup of eight tiles; about 512
 // workgroups, split-K (SwiGLU then finishes in k_split_reduce; the argmax never splits).
-template <typename T, int EPI>
+template <typename T, int EPI, bool NX = false>
 static int gemm_wide(GemmArgs a, int max_split, int tag, Stream s, int* nsplit_out) {
   const int ntiles = skinny_tiles(a.N);
   const int TN = a.N / (16 * ntiles);
@@ -1068,9 +1126,9 @@ static int gemm_wide(GemmArgs a, int max_split, int tag, Stream s, int* nsplit_o
 #define HAM_WIDE(MTV, TNV)                                                                              \
     do {                                                                                                \
       if (!tag && (EPI == EPI_F32 || EPI == EPI_RESID || EPI == EPI_SWIGLU))                            \
-        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 0>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
+        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 0, NX>), grid, dim3(64 * WIDE_NW), 0, s, a);            \
       else                                                                                              \
-        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 1>), grid, dim3(64 * WIDE_NW), 0, s, a);                \
+        launch_k((k_gemm_wide<T, MTV, TNV, EPI, 1, NX>), grid, dim3(64 * WIDE_NW), 0, s, a);            \
     } while (0)
     if (TN == 2) {
       if (mt <= 2) HAM_WIDE(2, 2); else if (mt <= 4) HAM_WIDE(4, 2); else if (mt <= 8) HAM_WIDE(8, 2);
@@ -1091,6 +1149,16 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
   constexpr int KB = Frag<T>::KB;
   if (a.N % 32 != 0 || a.K % KB != 0 || a.M <= 0) return -1;
   *nsplit_out = 1;
+  if (a.xsrc == XS_NORMW) {  // normed X built by the batched GEMM itself (8 < M <= 256)
+    if constexpr (EPI == EPI_F32 || EPI == EPI_SWIGLU) {
+      if (a.M > 8 && a.M <= 256 && a.K % WIDE_KC == 0 && a.xs.x && a.xs.g && a.xs.ssw &&
+          a.xs.nchw == (a.K + 255) / 256) {
+        if (dry) return 0;
+        return gemm_wide<T, EPI, true>(a, max_split, tag, s, nsplit_out);
+      }
+    }
+    return GEMM_NO_STAGE;
+  }
   if (a.xsrc != XS_ACT) {
     if constexpr (EPI == EPI_F32 || EPI == EPI_SWIGLU || EPI == EPI_RESID)
       return gemm_staged<T, EPI>(a, max_split, tag, s, nsplit_out, dry);

@@ -130,6 +130,16 @@ __global__ __launch_bounds__(256) void k_norm_scale(NormArgs a) {
   }
 }
 
+int launch_norm_reduce(const NormArgs& a, Stream s) {
+  // first phase only (x += partials, ctx copy, chunk sums of squares): the
+  // batched GEMM that consumes the rows applies 1/rms and the gain itself
+  if (a.R < NORM2_MIN_ROWS || a.R > NORM2_MAX_ROWS || !a.ss || a.row_stride != 1 || a.row_off != 0 || a.hid)
+    return -1;
+  if (a.part && (a.nsplit < 1 || a.nsplit > NORM_MAXS)) return -1;
+  launch_k(k_norm_reduce, dim3((a.d + 255) / 256, a.R), dim3(256), 0, s, a);
+  return 0;
+}
+
 int launch_rmsnorm(int dtype, const NormArgs& a, Stream s) {
   if (a.R <= 0) return 0;
   if (a.d > NORM_THREADS * NORM_MAXV || (a.part && (a.nsplit < 1 || a.nsplit > NORM_MAXS))) return -1;

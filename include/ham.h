@@ -63,9 +63,20 @@ extern "C" {
 typedef struct ham_config {
   /* base decoder (Llama family: RMSNorm, RoPE, GQA, SwiGLU; Sec. 4.1) */
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  /* compositional embedder (Sec. 3.2): one multi-head cross-attention layer
+   * followed by a linear map (Sec. 4.1); 1 (0 is read as 1) */
+  int32_t embed_layers;
   /* micro-step decoder: layers of the base configuration (Sec. 3.3) */
   int32_t micro_layers;
   int32_t max_group;    /* <= 4: micro-step cap (Sec. 3.6, Sec. 4.1) */
+  /* base layers whose residual outputs condition the micro decoder (Sec. 3.3,
+   * Fig. 2a: several middle layers' hidden states, the last included).
+   * n_ctx_layers = 0: C = min(4, n_layers) layers l_i = ceil(i * n_layers / C).
+   * Otherwise C = n_ctx_layers in 1..8 and ctx_layers[0..C) are 1-based layer
+   * indices, strictly increasing, each in 1..n_layers.  The micro decoder sees
+   * them as C prefix rows at local positions 0..C-1. */
+  int32_t n_ctx_layers;
+  int32_t ctx_layers[8];
   int32_t stop_mode;    /* HAM_STOP_* */
   int32_t stop_id;      /* TOKEN mode reserved id */
   float stop_conf;      /* HEAD mode confidence c in [0, 1] */

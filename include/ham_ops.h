@@ -1,10 +1,15 @@
 /*
  * libham single-kernel entry points, for parity tests and diagnostics.
  *
- * They run the same kernels as ham_macro_step on caller-provided buffers, so a
- * test can check one step of the decode loop at shapes where running the whole
- * model through a CPU reference is too slow (e.g. attention over a 32K-slot
- * cache).  Same conventions as include/ham.h: C functions, HAM_OK or a negative
+ * They run one kernel of the decode loop on caller-provided buffers, so a test
+ * can check one step at shapes where running the whole model through a CPU
+ * reference is too slow (e.g. attention over a 32K-slot cache):
+ *  - ham_op_attention_step runs the fused decode-attention step that every
+ *    base layer of ham_macro_step launches, with the same split choice for the
+ *    same batch and slot bound;
+ *  - ham_op_decode_attention runs the attention over an already filled cache
+ *    that the micro decoder's first step uses (a different kernel).
+ * Same conventions as include/ham.h: C functions, HAM_OK or a negative
  * HAM_E* code, ham_last_error() for the message, "d_" = device pointers, work
  * enqueued on `hip_stream` and valid after it is synchronised.
  *
@@ -44,6 +49,43 @@ int ham_op_decode_attention(int32_t dtype, int32_t rows, int32_t n_heads, int32_
                             int32_t slots_cap, const void* d_q, const void* d_k, const void* d_vt,
                             const int32_t* d_kv_len, const int32_t* d_enable, int32_t kv_max, void* d_out,
                             void* d_workspace, size_t workspace_bytes, void* hip_stream);
+
+/* The fused decode-attention step of one base layer of a macro-step (Sec. 3.1:
+ * the fused group's single new KV entry is appended, then attention runs over
+ * the smashed cache), for one row per sequence:
+ *   q = RoPE(q part of qkv[r]), k = RoPE(k part), v = v part, rotate-half RoPE
+ *   with the row's factors (pair (i, i + hd/2) rotated by cos[r][i], sin[r][i]);
+ *   k and v are rounded to the cache type and written at slot new_slot[r];
+ *   out[r, h] = sum_j softmax_j(q_h . K[r, h/(H/Hkv), j] / sqrt(hd)) V[..., j]
+ *   over slots j < kv_len[r] (the new slot included; its score uses the
+ *   rounded k).
+ *  d_qkv        fp32 [rows][(n_heads + 2*n_kv_heads)*head_dim]: all q heads,
+ *               then the k heads, then the v heads (before RoPE)
+ *  d_cos, d_sin fp32 [rows][head_dim/2]
+ *  d_k, d_vt    caches laid out as for ham_op_decode_attention; slot new_slot[r]
+ *               is written, slots below it are read
+ *  d_kv_len     int32 [rows]: slots after the append; d_new_slot int32 [rows]
+ *               must equal kv_len - 1 and be <= kv_cap, else the row writes
+ *               nothing, gets zeros and d_err[r] is OR-ed with 8
+ *  d_enable     int32 [rows]: 0 = the row writes nothing and gets zeros
+ *  kv_cap       host bound on new_slot for every row, < slots_cap; it and `rows`
+ *               choose the slot split exactly as a macro-step over `rows`
+ *               sequences does (ham_op_attention_step_splits tells how many)
+ *  d_err        int32 [rows], in/out (bits are only set)
+ *  d_out        act rows [rows][n_heads*head_dim]
+ *  d_workspace  at least ham_op_attention_workspace_bytes(rows, ...) bytes
+ * rows in 1..64, head_dim 64 or 128, n_heads/n_kv_heads in 1..4, slots_cap a
+ * multiple of 64.  HAM_EINVAL on a bad shape or null pointer, HAM_ENOMEM if
+ * the workspace is too small. */
+int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                          int32_t slots_cap, const float* d_qkv, const float* d_cos, const float* d_sin, void* d_k,
+                          void* d_vt, const int32_t* d_kv_len, const int32_t* d_new_slot, const int32_t* d_enable,
+                          int32_t kv_cap, int32_t* d_err, void* d_out, void* d_workspace, size_t workspace_bytes,
+                          void* hip_stream);
+
+/* Slot splits (workgroups per row and kv head) that ham_op_attention_step and
+ * a macro-step over `rows` sequences use for this slot bound; 0 if invalid. */
+int ham_op_attention_step_splits(int32_t dtype, int32_t rows, int32_t n_kv_heads, int32_t head_dim, int32_t kv_cap);
 
 #ifdef __cplusplus
 }

@@ -41,20 +41,28 @@ def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray, n_valid: Sequence[int], 
     """GQA softmax attention: q [T][H][hd]; K, V [S][Hkv][hd]; row t sees slots < n_valid[t];
     q-head h reads kv-head h // (H / Hkv); scores scaled by 1/sqrt(hd)."""
     T, H, hd = q.shape
-    kv_of = np.arange(H) // (H // n_kv_heads)
+    grp = H // n_kv_heads
     out = np.zeros((T, H, hd))
     scale = 1.0 / math.sqrt(hd)
-    for t in range(T):
-        n = int(n_valid[t])
+    n_valid = np.asarray(n_valid, dtype=np.int64).reshape(T)
+    # Rows are independent: they are taken in groups only to bound the size of
+    # the score matrix.  Within a row, a slot j counts iff j < n_valid[t].
+    ROWS = 512
+    for t0 in range(0, T, ROWS):
+        t1 = min(T, t0 + ROWS)
+        n = int(n_valid[t0:t1].max(initial=0))
         if n == 0:
             continue
-        Kh = K[:n][:, kv_of, :].astype(np.float64)    # [n][H][hd]
-        Vh = V[:n][:, kv_of, :].astype(np.float64)
-        sc = np.einsum("hd,nhd->hn", q[t], Kh) * scale
-        sc = sc - sc.max(axis=1, keepdims=True)
-        a = np.exp(sc)
-        a /= a.sum(axis=1, keepdims=True)
-        out[t] = np.einsum("hn,nhd->hd", a, Vh)
+        seen = np.arange(n)[None, :] < n_valid[t0:t1, None]         # [rows][n]
+        live = n_valid[t0:t1] > 0
+        for h in range(H):
+            Kh = K[:n, h // grp, :].astype(np.float64)               # [n][hd]
+            Vh = V[:n, h // grp, :].astype(np.float64)
+            sc = np.where(seen, (q[t0:t1, h, :] @ Kh.T) * scale, -np.inf)
+            m = np.where(live, sc.max(axis=1), 0.0)[:, None]
+            a = np.exp(sc - m)
+            a /= np.where(live, a.sum(axis=1), 1.0)[:, None]
+            out[t0:t1, h, :] = a @ Vh
     return out
 
 

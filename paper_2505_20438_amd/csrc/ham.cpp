@@ -65,7 +65,7 @@ size_t attn_part_bytes(int R, int H, int Hk, int hd);
 struct Layout {
   // dims
   int L, M, d, H, Hk, hd, F, V, G, B, P, steps;
-  int QKV, HD, Vpad, S, max_pos, C, Tc, rows_dec, rows_max, Nmax, ctx_l[4];
+  int QKV, HD, Vpad, S, max_pos, C, Tc, rows_dec, rows_max, Nmax, ctx_l[8];
   size_t es;  // element size of the storage type
   // weights
   size_t E, Pe, Aqkv, Ao, Alin, Wlm, gf, gmf, cos_t, sin_t, w_bytes;
@@ -87,6 +87,12 @@ const char* check_cfg(const ham_config* c) {
   if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32 || c->ffn_dim % 32) return "d_model, n_heads*head_dim and ffn_dim must be multiples of 32";
   if (c->d_model > 8192) return "d_model must be <= 8192";
   if (c->max_group < 1 || c->max_group > 4) return "max_group must be in 1..4";
+  if (c->embed_layers != 0 && c->embed_layers != 1) return "embed_layers must be 1 (one cross-attention layer)";
+  if (c->n_ctx_layers < 0 || c->n_ctx_layers > 8) return "n_ctx_layers must be in 0..8";
+  for (int i = 0; i < c->n_ctx_layers; ++i) {
+    if (c->ctx_layers[i] < 1 || c->ctx_layers[i] > c->n_layers) return "ctx_layers must lie in 1..n_layers";
+    if (i > 0 && c->ctx_layers[i] <= c->ctx_layers[i - 1]) return "ctx_layers must be strictly increasing";
+  }
   if (c->stop_mode < 0 || c->stop_mode > 3) return "unknown stop_mode";
   if (c->stop_mode == HAM_STOP_TOKEN && (c->stop_id < 0 || c->stop_id >= c->vocab)) return "stop_id out of range";
   if (!(c->stop_conf >= 0.f && c->stop_conf <= 1.f)) return "stop_conf must be in [0, 1]";
@@ -109,8 +115,13 @@ Layout make_layout(const ham_config* c) {
   y.Vpad = rup(y.V + 1, 32);
   y.S = rup(y.P + y.steps, 64);
   y.max_pos = y.P + y.G * (y.steps + 1) + 8;
-  y.C = std::min(4, y.L);
-  for (int i = 0; i < 4; ++i) y.ctx_l[i] = i < y.C ? (int)((long long)(i + 1) * y.L + y.C - 1) / y.C : -1;
+  // context layers of the micro decoder: the configured set, or C = min(4, L)
+  // layers at ceil(i * L / C), i = 1..C (evenly spaced, the last one included)
+  y.C = c->n_ctx_layers > 0 ? c->n_ctx_layers : std::min(4, y.L);
+  for (int i = 0; i < 8; ++i)
+    y.ctx_l[i] = i >= y.C ? -1
+                 : c->n_ctx_layers > 0 ? c->ctx_layers[i]
+                                       : (int)(((long long)(i + 1) * y.L + y.C - 1) / y.C);
   y.Tc = std::min(y.P, 2048);
   y.rows_dec = y.B * (y.C + 1);
   y.rows_max = std::max(y.Tc, std::max(y.rows_dec, 5 * y.B));
@@ -386,6 +397,14 @@ int attn_step_splits(int dtype, int R, int Hk, int hd, int kv_cap) {
   const int blocks = (kv_cap + kb - 1) / kb;
   const int for_width = std::min((256 + R * Hk - 1) / (R * Hk), (blocks + 1) / 2);
   return std::max(1, std::min(MAX_ATTN_SPLIT, for_width));
+}
+
+// splits of the base layers' fused step in a macro-step over B sequences: at
+// most 16 while the batch is small enough for the o-projection's prologue to
+// merge them (more would need a separate combine launch)
+int macro_attn_splits(int dtype, int B, int Hk, int hd, int kv_cap) {
+  const int n = attn_step_splits(dtype, B, Hk, hd, kv_cap);
+  return B <= 8 ? std::min(16, n) : n;
 }
 
 // one transformer layer (base layer j < L, micro layer j >= L) over R rows.
@@ -911,10 +930,7 @@ int macro_step_body(ham_model* m, int32_t* d_out_tokens, int32_t* d_out_lens) {
   // can hold, so every macro-step launches the same kernels with the same
   // arguments (graph replay); each row attends over its own device-side length
   const int kv_cap = std::min(m->prompt_len + y.steps - 1, y.S - 1);
-  // at most 16 splits while the batch is small enough for the o-projection's
-  // prologue to merge them (more would need a separate combine launch)
-  const int nsplit = B <= 8 ? std::min(16, attn_step_splits(dt, B, y.Hk, y.hd, kv_cap))
-                            : attn_step_splits(dt, B, y.Hk, y.hd, kv_cap);
+  const int nsplit = macro_attn_splits(dt, B, y.Hk, y.hd, kv_cap);
   const StepAttn bstep{m->WS<float>(y.rope_cs), m->WS<float>(y.rope_cs) + y.hd / 2, y.hd, kv_cap};
   float* ctx = m->WS<float>(y.ctx);
   Pending pend;
@@ -1106,6 +1122,44 @@ int ham_op_decode_attention(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, 
   if (launch_attn_decode(dtype, aa, (hipStream_t)stream)) return fail(HAM_EINVAL, "attention shape");
   HIP_TRY(hipGetLastError());
   return HAM_OK;
+}
+
+int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, int32_t hd, int32_t S,
+                          const float* d_qkv, const float* d_cos, const float* d_sin, void* d_k, void* d_vt,
+                          const int32_t* d_kv_len, const int32_t* d_new_slot, const int32_t* d_enable,
+                          int32_t kv_cap, int32_t* d_err, void* d_out, void* d_ws, size_t ws_bytes, void* stream) {
+  if (dtype != HAM_F32 && dtype != HAM_BF16) return fail(HAM_EINVAL, "bad dtype");
+  if (rows < 1 || rows > 64 || H < 1 || Hk < 1 || H % Hk || H / Hk > 4 || (hd != 64 && hd != 128) || S < 64 ||
+      S % 64)
+    return fail(HAM_EINVAL, "bad attention shape");
+  if (kv_cap < 0 || kv_cap >= S) return fail(HAM_EINVAL, "kv_cap out of range");
+  if (!d_qkv || !d_cos || !d_sin || !d_k || !d_vt || !d_kv_len || !d_new_slot || !d_enable || !d_err || !d_out ||
+      !d_ws)
+    return fail(HAM_EINVAL, "null pointer");
+  if (ws_bytes < attn_part_bytes(rows, H, Hk, hd)) return fail(HAM_ENOMEM, "workspace too small");
+  SeqPtrs sp{};
+  sp.kv_len = const_cast<int*>(d_kv_len);
+  sp.cur_slot = const_cast<int*>(d_new_slot);
+  sp.cur_pos = sp.cur_slot;  // read by the row map, unused by attention (RoPE factors are given)
+  sp.step_on = const_cast<int*>(d_enable);
+  sp.err = d_err;
+  AttnStepArgs sa{};
+  sa.qkv = d_qkv; sa.part = nullptr; sa.nsplit_qkv = 1; sa.pM = rows; sa.ldqkv = (H + 2 * Hk) * hd;
+  sa.cos_p = d_cos; sa.sin_p = d_sin; sa.cs_stride = hd / 2;
+  sa.K = d_k; sa.VT = d_vt; sa.sb = (long long)Hk * S * hd; sa.sh = (long long)S * hd; sa.S = S;
+  sa.H = H; sa.Hkv = Hk; sa.hd = hd; sa.R = rows; sa.kv_cap = kv_cap;
+  sa.nsplit = macro_attn_splits(dtype, rows, Hk, hd, kv_cap);
+  sa.o = d_out; sa.ldo = H * hd; sa.part_out = (float*)d_ws; sa.combine = true;
+  sa.ss = nullptr; sa.ss_n = 0; sa.d = 1; sa.eps = 0.f;
+  sa.rm.mode = ROWS_DECODE; sa.rm.st = sp;
+  if (launch_attn_step(dtype, sa, (hipStream_t)stream)) return fail(HAM_EINVAL, "attention step shape");
+  HIP_TRY(hipGetLastError());
+  return HAM_OK;
+}
+
+int ham_op_attention_step_splits(int32_t dtype, int32_t rows, int32_t Hk, int32_t hd, int32_t kv_cap) {
+  if ((dtype != HAM_F32 && dtype != HAM_BF16) || rows < 1 || Hk < 1 || kv_cap < 0) return 0;
+  return macro_attn_splits(dtype, rows, Hk, hd, kv_cap);
 }
 
 }  // extern "C"

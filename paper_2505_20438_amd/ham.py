@@ -22,13 +22,15 @@ HAM_PROF_KINDS = 9
 EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
             "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
             "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
-            "ham_op_attention_workspace_bytes", "ham_op_decode_attention")
+            "ham_op_attention_workspace_bytes", "ham_op_decode_attention", "ham_op_attention_step",
+            "ham_op_attention_step_splits")
 
 
 class HamConfig(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "vocab",
-        "micro_layers", "max_group", "stop_mode", "stop_id")] + [
+        "embed_layers", "micro_layers", "max_group", "n_ctx_layers")] + [
+        ("ctx_layers", ctypes.c_int32 * 8)] + [(n, ctypes.c_int32) for n in ("stop_mode", "stop_id")] + [
         ("stop_conf", ctypes.c_float), ("rope_theta", ctypes.c_float), ("norm_eps", ctypes.c_float),
         ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_prompt", ctypes.c_int32),
         ("max_steps", ctypes.c_int32)]
@@ -87,6 +89,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_op_attention_workspace_bytes.restype = SZ
     lib.ham_op_decode_attention.argtypes = [I32, I32, I32, I32, I32, I32, P, P, P, P, P, I32, P, P, SZ, P]
     lib.ham_op_decode_attention.restype = I32
+    lib.ham_op_attention_step.argtypes = [I32, I32, I32, I32, I32, I32, P, P, P, P, P, P, P, P, I32, P, P, P, SZ, P]
+    lib.ham_op_attention_step.restype = I32
+    lib.ham_op_attention_step_splits.argtypes = [I32, I32, I32, I32, I32]
+    lib.ham_op_attention_step_splits.restype = I32
     lib.ham_last_error.restype = ctypes.c_char_p
     lib.ham_destroy.argtypes = [P]
     lib.ham_destroy.restype = None
@@ -107,9 +113,16 @@ _check = check
 
 def make_config(**kw) -> HamConfig:
     c = HamConfig()
-    defaults = dict(max_group=4, stop_mode=HAM_STOP_FORCED, stop_id=0, stop_conf=0.5, rope_theta=500000.0,
-                    norm_eps=1e-5, dtype=HAM_BF16, max_batch=1, max_prompt=1, max_steps=0)
+    defaults = dict(embed_layers=1, max_group=4, stop_mode=HAM_STOP_FORCED, stop_id=0, stop_conf=0.5,
+                    rope_theta=500000.0, norm_eps=1e-5, dtype=HAM_BF16, max_batch=1, max_prompt=1, max_steps=0,
+                    ctx_layers=())
     defaults.update(kw)
+    layers = [int(x) for x in defaults.pop("ctx_layers")]
+    if len(layers) > 8:
+        raise ValueError("at most 8 context layers")
+    c.n_ctx_layers = len(layers)
+    for i, l in enumerate(layers):
+        c.ctx_layers[i] = l
     for k, v in defaults.items():
         setattr(c, k, v)
     return c
@@ -196,6 +209,21 @@ def ham_op_decode_attention(dtype: int, q, k, vt, kv_len, enable, kv_max: int, o
         dtype, rows, n_heads, n_kv_heads, head_dim, slots_cap, q.data_ptr(), k.data_ptr(), vt.data_ptr(),
         kv_len.data_ptr(), enable.data_ptr(), kv_max, out.data_ptr(), workspace.data_ptr(),
         workspace.numel() * workspace.element_size(), stream))
+
+
+def ham_op_attention_step(dtype: int, qkv, cos, sin, k, vt, kv_len, new_slot, enable, kv_cap: int, err, out,
+                          workspace, stream: int, n_heads: int, n_kv_heads: int, head_dim: int,
+                          slots_cap: int) -> None:
+    """Fused decode-attention step of one base layer, one row per sequence (include/ham_ops.h)."""
+    rows = kv_len.numel()
+    check(load_library().ham_op_attention_step(
+        dtype, rows, n_heads, n_kv_heads, head_dim, slots_cap, qkv.data_ptr(), cos.data_ptr(), sin.data_ptr(),
+        k.data_ptr(), vt.data_ptr(), kv_len.data_ptr(), new_slot.data_ptr(), enable.data_ptr(), kv_cap,
+        err.data_ptr(), out.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(), stream))
+
+
+def ham_op_attention_step_splits(dtype: int, rows: int, n_kv_heads: int, head_dim: int, kv_cap: int) -> int:
+    return load_library().ham_op_attention_step_splits(dtype, rows, n_kv_heads, head_dim, kv_cap)
 
 
 def ham_op_attention_workspace_bytes(rows: int, n_heads: int, n_kv_heads: int, head_dim: int) -> int:

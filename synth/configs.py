@@ -1,10 +1,10 @@
 """Model and workload shapes of the five benchmark configurations.
 
 Shapes only (no arithmetic).  ``ctx_layers`` are 1-based indices of the base
-layers whose residual outputs form the micro-decoder context: C = min(4, L)
-layers, l_i = ceil(i * L / C) (the paper conditions the micro decoder on several
-middle-layer hidden states including the last one, Sec. 3.3 and Fig. 2a; the
-choice of layers is this build's reading).
+layers whose residual outputs form the micro-decoder context: by default
+C = min(4, L) layers, l_i = ceil(i * L / C), or an explicit ``ctx_layer_set``
+(the paper conditions the micro decoder on several middle-layer hidden states,
+the last one included, Sec. 3.3 and Fig. 2a; the choice of layers is a reading).
 """
 from __future__ import annotations
 
@@ -32,9 +32,12 @@ class HamShape:
     rope_theta: float = 500000.0
     norm_eps: float = 1e-5
     dtype: int = BF16
+    ctx_layer_set: tuple = ()   # explicit 1-based context layers; empty = the default reading
 
     @property
     def ctx_layers(self) -> tuple:
+        if self.ctx_layer_set:
+            return tuple(int(x) for x in self.ctx_layer_set)
         c = min(4, self.n_layers)
         return tuple(int(math.ceil(i * self.n_layers / c)) for i in range(1, c + 1))
 

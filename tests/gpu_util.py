@@ -31,7 +31,7 @@ def config_for(shape: HamShape, batch: int, prompt: int, steps: int):
         head_dim=shape.head_dim, ffn_dim=shape.ffn_dim, vocab=shape.vocab, micro_layers=shape.micro_layers,
         max_group=shape.max_group, stop_mode=shape.stop_mode, stop_id=shape.stop_id, stop_conf=shape.stop_conf,
         rope_theta=shape.rope_theta, norm_eps=shape.norm_eps, dtype=shape.dtype, max_batch=batch,
-        max_prompt=prompt, max_steps=steps)
+        max_prompt=prompt, max_steps=steps, ctx_layers=shape.ctx_layer_set)
 
 
 @dataclasses.dataclass
@@ -129,3 +129,104 @@ def oracle_groups_for(om, prompts, budgets, steps, sched=None, record=False):
         forced = (lambda st, b=b: int(sched[b, st])) if sched is not None else None
         out.append(om.generate(prompts[b], int(budgets[b]), steps, forced=forced, record=record))
     return out
+
+
+def act_rows(torch, x, dtype):
+    """fp32 rows -> the library's activation layout (bf16 hi/lo planes for bf16)."""
+    if dtype == 0:
+        return x.contiguous()
+    hi = x.to(torch.bfloat16)
+    lo = (x - hi.float()).to(torch.bfloat16)
+    return torch.cat([hi, lo], dim=1).contiguous()
+
+
+def from_act(torch, buf, width, dtype):
+    """The library's activation layout -> fp32 rows."""
+    if dtype == 0:
+        return buf.float()
+    return buf[:, :width].float() + buf[:, width:].float()
+
+
+def tiled_v(torch, V):
+    """V [R][Hkv][S][hd] -> the cache's 32-slot tiles, d-major inside a tile: [R][Hkv][S/32][hd][32]."""
+    R, Hk, S, hd = V.shape
+    return V.reshape(R, Hk, S // 32, 32, hd).transpose(3, 4).contiguous()
+
+
+def untiled_v(torch, VT):
+    R, Hk, nt, hd, _ = VT.shape
+    return VT.transpose(3, 4).reshape(R, Hk, nt * 32, hd)
+
+
+def synthetic_groups(seed: int, sched_row, steps: int, vocab: int) -> List[List[int]]:
+    """Teacher groups for a row the oracle does not follow: the forced lengths,
+    seeded uniform token ids (any valid input will do for such a row)."""
+    ids = synth.prompt_ids(seed, 1, 4 * (steps + 1), vocab)[0]
+    return [[int(t) for t in ids[4 * st: 4 * st + int(sched_row[st])]] for st in range(steps + 1)]
+
+
+def teacher_forced(om, shp, prompts, budgets, steps, sched, seed, debug_steps, check_rows=None, cap_steps=None):
+    """Teacher-forced parity: the oracle runs free on ``check_rows`` (all rows by
+    default); the GPU is fed the oracle's groups on those rows (and seeded
+    synthetic groups of the forced lengths, unbudgeted, on the others), and every
+    captured decision of a checked row is compared: logits and normed hidden
+    within the tolerance, tokens exact or an explained near tie, group boundaries
+    and KV counts exact.  ``cap_steps`` sets the model's macro-step capacity
+    (default ``steps``), which fixes the decode-attention launch shape.
+    Returns (exact decisions, accepted near ties)."""
+    from paper_2505_20438_amd import ham
+    B = prompts.shape[0]
+    rows = list(range(B)) if check_rows is None else list(check_rows)
+    orc_of = {}
+    for b in rows:
+        forced = (lambda st, b=b: int(sched[b, st]))
+        orc_of[b] = om.generate(prompts[b], int(budgets[b]), steps, forced=forced, record=True)
+    teacher = []
+    for b in range(B):
+        if b in orc_of:
+            teacher.append(orc_of[b].groups)
+        else:
+            assert budgets[b] == 0, "rows the oracle does not follow run unbudgeted"
+            teacher.append(synthetic_groups(9000 + b, sched[b], steps, shp.vocab))
+    cfg = config_for(shp, B, prompts.shape[1], steps if cap_steps is None else cap_steps)
+    rt = ham.HamRuntime(cfg, seed)
+    res = run_gpu(rt, prompts, budgets, steps, sched, teacher=teacher, debug_steps=debug_steps)
+    tol = TOL[shp.dtype]
+    ties = exact = 0
+    errs = []
+    for b, o in orc_of.items():
+        decs = {(d.step, d.k): d for d in o.decisions}
+        for (bb, step, k), lg in res.logits.items():
+            if bb == b:
+                d = decs[(step, k)]
+                errs.append((float(np.max(np.abs(lg - d.logits))),
+                             float(np.max(np.abs(res.hidden[(b, step, k)] - d.h))),
+                             float(np.sqrt(np.mean((res.hidden[(b, step, k)] - d.h) ** 2))), b, step, k))
+    e = np.array([x[:3] for x in errs])
+    print("decisions", len(errs), "logit err max/mean", e[:, 0].max(), e[:, 0].mean(),
+          "hidden max/mean", e[:, 1].max(), e[:, 1].mean(), "hidden rms mean", e[:, 2].mean(), flush=True)
+    for x in sorted(errs, key=lambda x: -x[1])[:8]:
+        print("  worst", x)
+    for b, o in orc_of.items():
+        decs = {(d.step, d.k): d for d in o.decisions}
+        assert len(res.own[b]) == len(o.groups)
+        for step, toks in enumerate(res.own[b]):
+            assert len(toks) == len(o.groups[step])          # group boundaries exact
+            for k, t in enumerate(toks):
+                lg = res.logits.get((b, step, k))
+                if lg is not None:
+                    d = decs[(step, k)]
+                    assert np.max(np.abs(lg - d.logits)) <= tol, (b, step, k)
+                    assert np.max(np.abs(res.hidden[(b, step, k)] - d.h)) <= tol, (b, step, k)
+                    assert abs(res.stop[(b, step, k)] - d.stop_logit) <= tol, (b, step, k)
+                r = check_decision(decs[(step, k)], t, lg, tol)
+                ties += r == "near_tie"
+                exact += r == "exact"
+        st = res.stats[b]
+        assert st["kv_len"] == o.kv_len and st["gen_slots"] == o.gen_slots and st["tokens"] == o.tokens
+        assert st["groups"] == len(o.groups) and st["device_error"] == 0
+    for b in range(B):
+        assert res.stats[b]["device_error"] == 0, b
+        if b not in orc_of:   # unfollowed rows: one KV entry per consumed group all the same
+            assert res.stats[b]["gen_slots"] == steps and res.stats[b]["kv_len"] == prompts.shape[1] + steps, b
+    return exact, ties

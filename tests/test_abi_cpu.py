@@ -69,6 +69,51 @@ def test_invalid_configs_are_rejected(lib, field, value):
     assert len(lib.ham_last_error()) > 0
 
 
+@pytest.mark.parametrize("n,layers,ok", [
+    (0, [], True), (1, [2], True), (2, [1, 2], True), (2, [2, 1], False), (2, [1, 1], False),
+    (1, [0], False), (1, [3], False), (9, [1] * 8, False), (-1, [], False)])
+def test_context_layer_sets_are_validated(lib, n, layers, ok):
+    # the micro decoder's context layers (Sec. 3.3): 1-based, strictly increasing, within the base depth
+    cfg = config_for(TINY, 1, 8, 4)   # two base layers
+    cfg.n_ctx_layers = n
+    for i, l in enumerate(layers):
+        cfg.ctx_layers[i] = l
+    assert (ham.ham_weights_bytes(cfg) > 0) == ok
+
+
+def test_embedder_is_one_layer(lib):
+    cfg = config_for(TINY, 1, 8, 4)
+    for v, ok in ((0, True), (1, True), (2, False)):
+        cfg.embed_layers = v
+        assert (ham.ham_weights_bytes(cfg) > 0) == ok
+
+
+def test_more_context_layers_grow_the_micro_workspace(lib):
+    base = config_for(SHAPE_1B, 4, 64, 8)
+    more = config_for(SHAPE_1B, 4, 64, 8)
+    more.n_ctx_layers = 8
+    for i in range(8):
+        more.ctx_layers[i] = 2 * i + 1
+    assert ham.ham_workspace_bytes(more) > ham.ham_workspace_bytes(base)
+
+
+def test_op_attention_step_rejects_bad_shapes(lib):
+    ws = ham.ham_op_attention_workspace_bytes(4, 32, 8, 128)
+    assert ham.ham_op_attention_step_splits(1, 4, 8, 128, 33791) == 8
+    assert ham.ham_op_attention_step_splits(1, 32, 8, 128, 2559) == 1
+    assert ham.ham_op_attention_step_splits(1, 1, 8, 64, 1023) == 16
+    assert ham.ham_op_attention_step_splits(5, 1, 8, 64, 1023) == 0
+    args = lambda rows, hd, S, cap, wsb: (1, rows, 32, 8, hd, S, *([256] * 8), cap, 256, 256, 256, wsb, None)  # noqa: E731
+    assert lib.ham_op_attention_step(*args(4, 96, 33792, 100, ws)) == ham.HAM_EINVAL        # head dim
+    assert lib.ham_op_attention_step(*args(4, 128, 100, 10, ws)) == ham.HAM_EINVAL          # slots not /64
+    assert lib.ham_op_attention_step(*args(4, 128, 33792, 33792, ws)) == ham.HAM_EINVAL     # kv_cap >= slots
+    assert lib.ham_op_attention_step(*args(65, 128, 33792, 100, ws)) == ham.HAM_EINVAL      # rows
+    assert lib.ham_op_attention_step(*args(4, 128, 33792, 100, 16)) == ham.HAM_ENOMEM       # workspace
+    a = list(args(4, 128, 33792, 100, ws))
+    a[8] = None   # no sin table
+    assert lib.ham_op_attention_step(*a) == ham.HAM_EINVAL
+
+
 def test_token_mode_stop_id_must_be_in_vocab(lib):
     cfg = config_for(TINY, 1, 8, 4)
     cfg.stop_id = TINY.vocab

@@ -10,7 +10,7 @@ import pytest
 import synth
 from oracle import OracleHam
 from synth.configs import BF16, SHAPE_1B, STOP_FORCED, STOP_FORCED_TOKEN, STOP_HEAD, STOP_TOKEN, TINY, WORKLOADS
-from tests.gpu_util import SMALL16, TOL, check_decision, config_for, oracle_groups_for, run_gpu
+from tests.gpu_util import SMALL16, TOL, check_decision, config_for, oracle_groups_for, run_gpu, teacher_forced
 
 pytestmark = pytest.mark.gpu
 
@@ -94,43 +94,7 @@ def test_tiny_fp32_free_running_exact(torch_cuda, mode):
 
 
 def _teacher_forced(om, shp, prompts, budgets, steps, sched, seed, debug_steps):
-    orcs = oracle_groups_for(om, prompts, budgets, steps, sched, record=True)
-    teacher = [o.groups for o in orcs]
-    rt = _runtime(shp, seed, prompts.shape[0], prompts.shape[1], steps)
-    res = run_gpu(rt, prompts, budgets, steps, sched, teacher=teacher, debug_steps=debug_steps)
-    tol = TOL[shp.dtype]
-    ties = exact = 0
-    errs = []
-    for b, o in enumerate(orcs):
-        decs = {(d.step, d.k): d for d in o.decisions}
-        for (bb, step, k), lg in res.logits.items():
-            if bb == b:
-                d = decs[(step, k)]
-                errs.append((float(np.max(np.abs(lg - d.logits))), float(np.max(np.abs(res.hidden[(b, step, k)] - d.h))),
-                             float(np.sqrt(np.mean((res.hidden[(b, step, k)] - d.h) ** 2))), b, step, k))
-    e = np.array([x[:3] for x in errs])
-    print("decisions", len(errs), "logit err max/mean", e[:, 0].max(), e[:, 0].mean(),
-          "hidden max/mean", e[:, 1].max(), e[:, 1].mean(), "hidden rms mean", e[:, 2].mean())
-    for x in sorted(errs, key=lambda x: -x[1])[:8]:
-        print("  worst", x)
-    for b, o in enumerate(orcs):
-        decs = {(d.step, d.k): d for d in o.decisions}
-        assert len(res.own[b]) == len(o.groups)
-        for step, toks in enumerate(res.own[b]):
-            assert len(toks) == len(o.groups[step])          # group boundaries exact
-            for k, t in enumerate(toks):
-                lg = res.logits.get((b, step, k))
-                if lg is not None:
-                    d = decs[(step, k)]
-                    assert np.max(np.abs(lg - d.logits)) <= tol, (b, step, k)
-                    assert np.max(np.abs(res.hidden[(b, step, k)] - d.h)) <= tol, (b, step, k)
-                r = check_decision(decs[(step, k)], t, lg, tol)
-                ties += r == "near_tie"
-                exact += r == "exact"
-        st = res.stats[b]
-        assert st["kv_len"] == o.kv_len and st["gen_slots"] == o.gen_slots and st["tokens"] == o.tokens
-        assert st["groups"] == len(o.groups) and st["device_error"] == 0
-    return exact, ties
+    return teacher_forced(om, shp, prompts, budgets, steps, sched, seed, debug_steps)
 
 
 def test_small_bf16_teacher_forced_ragged_batch(torch_cuda):
@@ -239,3 +203,16 @@ def test_head_c1_equals_one_token_decoding(torch_cuda):
         assert all(len(g) == 1 for g in res_h.groups[b])
         assert res_h.groups[b] == res_1.groups[b]
         assert res_h.stats[b]["kv_len"] == res_1.stats[b]["kv_len"] == P + steps
+
+
+@pytest.mark.parametrize("layers,dtype,B", [((1, 3), 0, 1), ((1, 2, 3, 5, 7, 8), BF16, 3)])
+def test_configured_context_layers_teacher_forced(torch_cuda, layers, dtype, B):
+    # a non-default set of base layers conditions the micro decoder (Sec. 3.3, Fig. 2a):
+    # C context rows at local positions 0..C-1, here C = 2 (fp32, one sequence) and C = 6
+    shp = dataclasses.replace(SMALL16, n_layers=4 if max(layers) <= 4 else 8, ctx_layer_set=layers, dtype=dtype)
+    P, steps = 40, 8
+    prompts = synth.prompt_ids(4020 + B, B, P, shp.vocab)
+    sched = synth.group_schedule(5020 + B, B, steps + 1, 4)
+    om = OracleHam(shp, 6020 + B)
+    exact, ties = teacher_forced(om, shp, prompts, [0] * B, steps, sched, 6020 + B, debug_steps=steps + 1)
+    assert ties == 0 if dtype == 0 else ties <= 1

@@ -158,3 +158,26 @@ def test_forced_token_costs_one_extra_micro_step_per_short_group():
     assert len(tok.decisions) == len(head.decisions) + extra
     for g, n_dec in zip(head.groups, np.bincount([d.step for d in tok.decisions])):
         assert n_dec == len(g) + (1 if len(g) < 4 else 0)
+
+
+@pytest.mark.parametrize("layers", [(1,), (2, 3), (1, 3)])
+def test_explicit_context_layers_match_reference_and_matter(layers):
+    # the micro decoder's context rows come from the configured base layers (Sec. 3.3,
+    # Fig. 2a): both readings follow the set, and a different set changes the decisions
+    shp = dataclasses.replace(SMALL, stop_mode=STOP_FORCED, ctx_layer_set=layers)
+    om, ref = OracleHam(shp, 33), RefHam(shp, 33)
+    prompt = _prompt(43, 10, shp.vocab)
+    sched = synth.group_schedule(53, 1, 64, 4)[0]
+    forced = lambda st: int(sched[st])  # noqa: E731
+    res = om.generate(prompt, 0, 6, forced=forced, record=True)
+    rec = []
+    assert res.groups == ref.generate(prompt, 0, 6, forced=forced, record=rec)
+    for d, (t, st, lg) in zip(res.decisions, rec):
+        assert np.allclose(d.logits, lg, rtol=1e-5, atol=1e-6)
+    default = OracleHam(dataclasses.replace(shp, ctx_layer_set=()), 33).generate(prompt, 0, 6, forced=forced,
+                                                                                 record=True)
+    micro = [(a.logits, b.logits) for a, b in zip(res.decisions, default.decisions) if a.k >= 1]
+    assert micro and all(not np.allclose(a, b) for a, b in micro)
+    # decisions from the base model (k = 0) do not depend on the context set
+    base = [(a.logits, b.logits) for a, b in zip(res.decisions, default.decisions) if a.k == 0]
+    assert all(np.array_equal(a, b) for a, b in base[:1])

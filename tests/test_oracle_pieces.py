@@ -143,3 +143,31 @@ def test_stop_threshold_readings():
                 assert cont == (s <= om.tau), (c, s)
     assert OracleHam(dataclasses.replace(SMALL, stop_conf=1.0), 1).tau == -math.inf
     assert OracleHam(dataclasses.replace(SMALL, stop_conf=0.0), 1).tau == math.inf
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+@pytest.mark.parametrize("rows,chunk", [(40000, 16384), (50, 7), (16384, 16384), (16385, 16384)])
+def test_uncached_matvec_row_chunks_match_the_plain_product(bf16, rows, chunk):
+    # Matrices too large to keep in float64 (the LM head at vocabulary 128256) are
+    # multiplied a block of rows at a time; the result must be the plain x @ W^T
+    # for every row, including a ragged last block.  W is expanded independently
+    # here (torch's bfloat16 view of the bit patterns).
+    from oracle.ham import _Mat
+    rng = np.random.default_rng(rows + 13 * bf16)
+    cols = 24
+    vals = rng.standard_normal(rows * cols).astype(np.float32)
+    if bf16:
+        data = torch.from_numpy(vals).bfloat16().view(torch.int16).numpy().view(np.uint16)
+        W = torch.from_numpy(data.view(np.int16)).view(torch.bfloat16).double().numpy().reshape(rows, cols)
+    else:
+        data = vals
+        W = vals.astype(np.float64).reshape(rows, cols)
+    m = _Mat(data.copy(), rows, cols, bf16)
+    assert m._f64 is None
+    x = rng.standard_normal((3, cols))
+    got = m.matvec(x, chunk=chunk)
+    ref = (torch.from_numpy(x) @ torch.from_numpy(W).T).numpy()
+    assert got.shape == (3, rows)
+    assert np.allclose(got, ref, rtol=1e-12, atol=1e-12)
+    # a planted slicing mistake (a block shifted by one row) would move whole rows
+    assert np.array_equal(np.argmax(got, axis=1), np.argmax(ref, axis=1))

@@ -195,6 +195,22 @@ int ham_set_debug(ham_model* m, void* d_buf, size_t bytes);
 /* Number of macro-steps run since the last prefill, or -1. */
 int ham_steps_done(const ham_model* m);
 
+/* Save and restore the decode state, so that one prefill can start several
+ * decodes (the benchmark times every generation from the same prefilled
+ * cache; a server could fork a sequence after a shared prompt).
+ * ham_state_save enqueues a device-to-device copy of the whole state buffer
+ * (the smashed KV cache and the per-sequence counters, ham_state_bytes bytes)
+ * into d_dst and records on the handle the batch, prompt length and macro-step
+ * count it belongs to.  ham_state_restore enqueues the copy back from d_src,
+ * which must hold what the last ham_state_save of this handle wrote, and
+ * resets those host-side fields, so later ham_macro_step calls continue from
+ * the saved point.  Both only enqueue work on the model's stream; the caller
+ * owns d_dst/d_src and keeps them unchanged in between.  HAM_ESTATE before the
+ * first prefill (save) or save (restore), HAM_ENOMEM if bytes <
+ * ham_state_bytes. */
+int ham_state_save(ham_model* m, void* d_dst, size_t bytes);
+int ham_state_restore(ham_model* m, const void* d_src, size_t bytes);
+
 /* Diagnostics: whether ham_macro_step replays its launches from a HIP graph
  * (enable = 1, the default) or launches each kernel on the stream (0).  The
  * graph holds every launch after the step's first kernel, captured once and

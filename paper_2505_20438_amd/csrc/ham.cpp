@@ -202,6 +202,8 @@ struct ham_model {
   hipStream_t s;
   SeqPtrs sp;
   int batch = 0, prompt_len = 0, steps_done = -1, has_teacher = 0, kv_visible = 0;
+  // host-side fields of the last ham_state_save (saved_steps < 0: none)
+  int saved_batch = 0, saved_prompt = 0, saved_steps = -1, saved_teacher = 0;
   float tau;
   float* dbg = nullptr;
   // optional per-class event timing
@@ -1058,6 +1060,30 @@ int ham_set_debug(ham_model* m, void* d_buf, size_t bytes) {
 }
 
 int ham_steps_done(const ham_model* m) { return m ? m->steps_done : -1; }
+
+int ham_state_save(ham_model* m, void* d_dst, size_t bytes) {
+  if (!m || !d_dst) return fail(HAM_EINVAL, "null argument");
+  if (m->steps_done < 0) return fail(HAM_ESTATE, "ham_state_save before ham_prefill");
+  if (bytes < m->y.st_bytes) return fail(HAM_ENOMEM, "state copy needs %zu bytes", m->y.st_bytes);
+  HIP_TRY(hipMemcpyAsync(d_dst, m->st, m->y.st_bytes, hipMemcpyDeviceToDevice, m->s));
+  m->saved_batch = m->batch;
+  m->saved_prompt = m->prompt_len;
+  m->saved_steps = m->steps_done;
+  m->saved_teacher = m->has_teacher;
+  return HAM_OK;
+}
+
+int ham_state_restore(ham_model* m, const void* d_src, size_t bytes) {
+  if (!m || !d_src) return fail(HAM_EINVAL, "null argument");
+  if (m->saved_steps < 0) return fail(HAM_ESTATE, "ham_state_restore before ham_state_save");
+  if (bytes < m->y.st_bytes) return fail(HAM_ENOMEM, "state copy needs %zu bytes", m->y.st_bytes);
+  HIP_TRY(hipMemcpyAsync(m->st, d_src, m->y.st_bytes, hipMemcpyDeviceToDevice, m->s));
+  m->batch = m->saved_batch;
+  m->prompt_len = m->saved_prompt;
+  m->steps_done = m->saved_steps;
+  m->has_teacher = m->saved_teacher;
+  return HAM_OK;
+}
 
 int ham_set_graph(ham_model* m, int enable) {
   if (!m) return fail(HAM_EINVAL, "null model");

@@ -23,7 +23,7 @@ EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_
             "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
             "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
             "ham_op_attention_workspace_bytes", "ham_op_decode_attention", "ham_op_attention_step",
-            "ham_op_attention_step_splits")
+            "ham_op_attention_step_splits", "ham_state_save", "ham_state_restore")
 
 
 class HamConfig(ctypes.Structure):
@@ -93,11 +93,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_op_attention_step.restype = I32
     lib.ham_op_attention_step_splits.argtypes = [I32, I32, I32, I32, I32]
     lib.ham_op_attention_step_splits.restype = I32
+    lib.ham_state_save.argtypes = [P, P, SZ]
+    lib.ham_state_restore.argtypes = [P, P, SZ]
     lib.ham_last_error.restype = ctypes.c_char_p
     lib.ham_destroy.argtypes = [P]
     lib.ham_destroy.restype = None
     for n in ("ham_init_weights", "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug",
-              "ham_steps_done", "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read"):
+              "ham_steps_done", "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read",
+              "ham_state_save", "ham_state_restore"):
         getattr(lib, n).restype = I32
     _lib = lib
     return lib
@@ -291,6 +294,14 @@ class HamRuntime:
 
     def macro_step(self, forced=None, teacher=None):
         ham_macro_step(self.handle, forced, teacher, self.out_tokens, self.out_lens)
+
+    def save_state(self, buf) -> None:
+        """Copy the decode state (KV cache + counters) into ``buf`` (uint8, >= state bytes)."""
+        _check(load_library().ham_state_save(self.handle, buf.data_ptr(), buf.numel() * buf.element_size()))
+
+    def restore_state(self, buf) -> None:
+        """Continue from the point of the last save_state (its copy in ``buf``)."""
+        _check(load_library().ham_state_restore(self.handle, buf.data_ptr(), buf.numel() * buf.element_size()))
 
     def set_graph(self, enable: bool) -> None:
         _check(load_library().ham_set_graph(self.handle, 1 if enable else 0))

@@ -37,7 +37,7 @@ import synth  # noqa: E402
 from oracle import OracleHam  # noqa: E402
 from synth.configs import WORKLOADS  # noqa: E402
 
-MACRO_STEPS = {"c2_1b_bf16": 24, "c3_8b_bf16": 3}
+MACRO_STEPS = {"c2_1b_bf16": 24, "c3_8b_bf16": 7}
 N_LOGITS, N_HIDDEN, TOP = 192, 96, 16
 
 

@@ -98,3 +98,27 @@ def test_seeded_schedules_match_the_expected_bytes(name):
     # one KV entry per group after the prefill's: about 1 / 1.875 per output token
     gen_slots = sum(len(l) - 1 for l in lens)
     assert gen_slots / (B * w.max_new) == pytest.approx(1 / mean_len, rel=0.06)
+
+
+def test_micro_steps_needed_counts_the_longest_group_of_the_running_rows():
+    w = _workload(2, 10, 6)
+    lens = [[4, 1, 3, 2], [2, 4]]            # row 1 finishes after macro-step 1
+    # step 1: groups 1 and 4 -> 3 micro steps; consumed 4 and 2 -> fused
+    # step 2: row 0 only, group 3 -> 2; consumed 1 -> not fused
+    # step 3: group 2 -> 1; consumed 3 -> fused
+    assert bench.micro_steps_needed(w, lens, 3) == (6, 2)
+    assert bench.micro_steps_needed(w, lens, 1) == (3, 1)
+
+
+def test_cost_model_of_sec_3_7_closed_forms():
+    # r = sum n C(S) / sum (C(S) + (n - 1) c): groups of one give r = 1 (the base model's
+    # own computation, Sec. 3.7 "Minimal Overhead"); full groups give 4 C / (C + 3 c) per step
+    w = _workload(1, 100, 12)
+    z = _sizes(w.shape)
+    assert bench.cost_model_speedup(w, [[1] * 13], 12) == pytest.approx(1.0, rel=1e-12)
+    lens = [[4, 4, 4]]
+    C = [z["base"] + z["lm"] + (100 + 1 + i) * z["slot"] for i in range(2)]
+    c = z["micro"] + z["lm"]
+    expect = sum(4 * x for x in C) / sum(x + 3 * c for x in C)
+    assert bench.cost_model_speedup(w, lens, 2) == pytest.approx(expect, rel=1e-12)
+    assert 1.0 < expect < 4.0

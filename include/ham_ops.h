@@ -83,6 +83,26 @@ int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t n_heads, int32_t 
                           int32_t kv_cap, int32_t* d_err, void* d_out, void* d_workspace, size_t workspace_bytes,
                           void* hip_stream);
 
+/* ham_op_attention_step without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the split records live in a library-owned device
+ * array of ham_op_attention_step_noalloc_max_bytes() bytes (4 MiB), one per
+ * GPU, kept until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); on its first use on a device it
+ * looks up that device's copy of the array (the current device).  Arguments,
+ * results and errors as for ham_op_attention_step, plus HAM_ENOMEM when the
+ * launch's split records (rows * n_kv_heads * splits * (n_heads/n_kv_heads) *
+ * (head_dim + 2) * 4 bytes, none when unsplit) exceed the array.  Every split
+ * writes its whole record before the merge reads it, so nothing needs
+ * clearing between calls; calls that overlap on one GPU (other streams or
+ * host threads) share the array and race. */
+int ham_op_attention_step_noalloc(int32_t dtype, int32_t rows, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                  int32_t slots_cap, const float* d_qkv, const float* d_cos, const float* d_sin,
+                                  void* d_k, void* d_vt, const int32_t* d_kv_len, const int32_t* d_new_slot,
+                                  const int32_t* d_enable, int32_t kv_cap, int32_t* d_err, void* d_out,
+                                  void* hip_stream);
+size_t ham_op_attention_step_noalloc_max_bytes(void);
+
 /* Slot splits (workgroups per row and kv head) that ham_op_attention_step and
  * a macro-step over `rows` sequences use for this slot bound; 0 if invalid. */
 int ham_op_attention_step_splits(int32_t dtype, int32_t rows, int32_t n_kv_heads, int32_t head_dim, int32_t kv_cap);

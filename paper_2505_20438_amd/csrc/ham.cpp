@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1150,19 +1151,64 @@ int ham_op_decode_attention(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, 
   return HAM_OK;
 }
 
-int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, int32_t hd, int32_t S,
+}  // extern "C"
+
+namespace {
+
+// Scratch of ham_op_attention_step_noalloc: the split records of the attention
+// step, at most NOALLOC_SCRATCH bytes, one copy per GPU for the life of the
+// process.  Host code reaches it only through the device address that
+// hipGetSymbolAddress returns for the current device (noalloc_scratch).
+constexpr size_t NOALLOC_SCRATCH = size_t(4) << 20;
+__device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH];
+
+std::mutex g_scratch_mu;
+constexpr int MAX_DEVICES = 64;
+void* g_scratch_dev[MAX_DEVICES] = {};
+
+int noalloc_scratch(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(HAM_EINVAL, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(HAM_EHIP, "no device address for the scratch array");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return HAM_OK;
+}
+
+// split-record bytes of one fused attention step launch (nothing when unsplit)
+size_t attn_step_record_bytes(int rows, int H, int Hk, int hd, int nsplit) {
+  return nsplit > 1 ? (size_t)rows * Hk * nsplit * (H / Hk) * (hd + 2) * 4 : 0;
+}
+
+int attention_step_common(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, int32_t hd, int32_t S,
                           const float* d_qkv, const float* d_cos, const float* d_sin, void* d_k, void* d_vt,
                           const int32_t* d_kv_len, const int32_t* d_new_slot, const int32_t* d_enable,
-                          int32_t kv_cap, int32_t* d_err, void* d_out, void* d_ws, size_t ws_bytes, void* stream) {
+                          int32_t kv_cap, int32_t* d_err, void* d_out, void* d_ws, size_t ws_bytes, bool noalloc,
+                          void* stream) {
   if (dtype != HAM_F32 && dtype != HAM_BF16) return fail(HAM_EINVAL, "bad dtype");
   if (rows < 1 || rows > 64 || H < 1 || Hk < 1 || H % Hk || H / Hk > 4 || (hd != 64 && hd != 128) || S < 64 ||
       S % 64)
     return fail(HAM_EINVAL, "bad attention shape");
   if (kv_cap < 0 || kv_cap >= S) return fail(HAM_EINVAL, "kv_cap out of range");
   if (!d_qkv || !d_cos || !d_sin || !d_k || !d_vt || !d_kv_len || !d_new_slot || !d_enable || !d_err || !d_out ||
-      !d_ws)
+      (!noalloc && !d_ws))
     return fail(HAM_EINVAL, "null pointer");
-  if (ws_bytes < attn_part_bytes(rows, H, Hk, hd)) return fail(HAM_ENOMEM, "workspace too small");
+  const int nsplit = macro_attn_splits(dtype, rows, Hk, hd, kv_cap);
+  if (noalloc) {
+    const size_t need = attn_step_record_bytes(rows, H, Hk, hd, nsplit);
+    if (need > NOALLOC_SCRATCH)
+      return fail(HAM_ENOMEM, "split records need %zu bytes, above the %zu-byte scratch of the allocation-free entry",
+                  need, NOALLOC_SCRATCH);
+    if (int rc = noalloc_scratch(&d_ws)) return rc;
+  } else if (ws_bytes < attn_part_bytes(rows, H, Hk, hd)) {
+    return fail(HAM_ENOMEM, "workspace too small");
+  }
   SeqPtrs sp{};
   sp.kv_len = const_cast<int*>(d_kv_len);
   sp.cur_slot = const_cast<int*>(d_new_slot);
@@ -1174,7 +1220,7 @@ int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, in
   sa.cos_p = d_cos; sa.sin_p = d_sin; sa.cs_stride = hd / 2;
   sa.K = d_k; sa.VT = d_vt; sa.sb = (long long)Hk * S * hd; sa.sh = (long long)S * hd; sa.S = S;
   sa.H = H; sa.Hkv = Hk; sa.hd = hd; sa.R = rows; sa.kv_cap = kv_cap;
-  sa.nsplit = macro_attn_splits(dtype, rows, Hk, hd, kv_cap);
+  sa.nsplit = nsplit;
   sa.o = d_out; sa.ldo = H * hd; sa.part_out = (float*)d_ws; sa.combine = true;
   sa.ss = nullptr; sa.ss_n = 0; sa.d = 1; sa.eps = 0.f;
   sa.rm.mode = ROWS_DECODE; sa.rm.st = sp;
@@ -1182,6 +1228,28 @@ int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, in
   HIP_TRY(hipGetLastError());
   return HAM_OK;
 }
+
+}  // namespace
+
+extern "C" {
+
+int ham_op_attention_step(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, int32_t hd, int32_t S,
+                          const float* d_qkv, const float* d_cos, const float* d_sin, void* d_k, void* d_vt,
+                          const int32_t* d_kv_len, const int32_t* d_new_slot, const int32_t* d_enable,
+                          int32_t kv_cap, int32_t* d_err, void* d_out, void* d_ws, size_t ws_bytes, void* stream) {
+  return attention_step_common(dtype, rows, H, Hk, hd, S, d_qkv, d_cos, d_sin, d_k, d_vt, d_kv_len, d_new_slot,
+                               d_enable, kv_cap, d_err, d_out, d_ws, ws_bytes, false, stream);
+}
+
+int ham_op_attention_step_noalloc(int32_t dtype, int32_t rows, int32_t H, int32_t Hk, int32_t hd, int32_t S,
+                                  const float* d_qkv, const float* d_cos, const float* d_sin, void* d_k, void* d_vt,
+                                  const int32_t* d_kv_len, const int32_t* d_new_slot, const int32_t* d_enable,
+                                  int32_t kv_cap, int32_t* d_err, void* d_out, void* stream) {
+  return attention_step_common(dtype, rows, H, Hk, hd, S, d_qkv, d_cos, d_sin, d_k, d_vt, d_kv_len, d_new_slot,
+                               d_enable, kv_cap, d_err, d_out, nullptr, 0, true, stream);
+}
+
+size_t ham_op_attention_step_noalloc_max_bytes(void) { return NOALLOC_SCRATCH; }
 
 int ham_op_attention_step_splits(int32_t dtype, int32_t rows, int32_t Hk, int32_t hd, int32_t kv_cap) {
   if ((dtype != HAM_F32 && dtype != HAM_BF16) || rows < 1 || Hk < 1 || kv_cap < 0) return 0;

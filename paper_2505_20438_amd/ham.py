@@ -23,7 +23,8 @@ EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_
             "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",
             "ham_tensor_info", "ham_set_graph", "ham_profile", "ham_profile_read", "ham_last_error", "ham_destroy",
             "ham_op_attention_workspace_bytes", "ham_op_decode_attention", "ham_op_attention_step",
-            "ham_op_attention_step_splits", "ham_state_save", "ham_state_restore")
+            "ham_op_attention_step_splits", "ham_state_save", "ham_state_restore", "ham_op_attention_step_noalloc",
+            "ham_op_attention_step_noalloc_max_bytes")
 
 
 class HamConfig(ctypes.Structure):
@@ -91,6 +92,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ham_op_decode_attention.restype = I32
     lib.ham_op_attention_step.argtypes = [I32, I32, I32, I32, I32, I32, P, P, P, P, P, P, P, P, I32, P, P, P, SZ, P]
     lib.ham_op_attention_step.restype = I32
+    lib.ham_op_attention_step_noalloc.argtypes = [I32, I32, I32, I32, I32, I32, P, P, P, P, P, P, P, P, I32, P, P, P]
+    lib.ham_op_attention_step_noalloc.restype = I32
+    lib.ham_op_attention_step_noalloc_max_bytes.argtypes = []
+    lib.ham_op_attention_step_noalloc_max_bytes.restype = SZ
     lib.ham_op_attention_step_splits.argtypes = [I32, I32, I32, I32, I32]
     lib.ham_op_attention_step_splits.restype = I32
     lib.ham_state_save.argtypes = [P, P, SZ]
@@ -223,6 +228,17 @@ def ham_op_attention_step(dtype: int, qkv, cos, sin, k, vt, kv_len, new_slot, en
         dtype, rows, n_heads, n_kv_heads, head_dim, slots_cap, qkv.data_ptr(), cos.data_ptr(), sin.data_ptr(),
         k.data_ptr(), vt.data_ptr(), kv_len.data_ptr(), new_slot.data_ptr(), enable.data_ptr(), kv_cap,
         err.data_ptr(), out.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(), stream))
+
+
+def ham_op_attention_step_noalloc(dtype: int, qkv, cos, sin, k, vt, kv_len, new_slot, enable, kv_cap: int, err,
+                                  out, stream: int, n_heads: int, n_kv_heads: int, head_dim: int,
+                                  slots_cap: int) -> None:
+    """ham_op_attention_step with its split records in the library's own device array."""
+    rows = kv_len.numel()
+    check(load_library().ham_op_attention_step_noalloc(
+        dtype, rows, n_heads, n_kv_heads, head_dim, slots_cap, qkv.data_ptr(), cos.data_ptr(), sin.data_ptr(),
+        k.data_ptr(), vt.data_ptr(), kv_len.data_ptr(), new_slot.data_ptr(), enable.data_ptr(), kv_cap,
+        err.data_ptr(), out.data_ptr(), stream))
 
 
 def ham_op_attention_step_splits(dtype: int, rows: int, n_kv_heads: int, head_dim: int, kv_cap: int) -> int:

@@ -216,3 +216,27 @@ def test_configured_context_layers_teacher_forced(torch_cuda, layers, dtype, B):
     om = OracleHam(shp, 6020 + B)
     exact, ties = teacher_forced(om, shp, prompts, [0] * B, steps, sched, 6020 + B, debug_steps=steps + 1)
     assert ties == 0 if dtype == 0 else ties <= 1
+
+
+def test_max_group_one_against_oracle_plain_decoding(torch_cuda):
+    # the base comparator (max group 1): no embedder fusion, no micro steps, one KV entry
+    # per token, i.e. the base model's own computation (Sec. 3.4; Sec. 3.7 "Minimal
+    # Overhead"), at the 1B layer shape and full vocabulary against the oracle's group-size-1
+    # run: teacher-forced on two sequences, then free-running on one
+    w = WORKLOADS["c2_1b_bf16"]
+    shp = dataclasses.replace(w.shape, n_layers=4, max_group=1)
+    B, P, steps = 2, 128, 24
+    prompts = synth.prompt_ids(4012, B, P, shp.vocab)
+    sched = np.ones((B, steps + 1), dtype=np.int32)
+    om = OracleHam(shp, 6012)
+    exact, ties = teacher_forced(om, shp, prompts, [0] * B, steps, sched, 6012, debug_steps=steps + 1)
+    assert ties <= 1 and exact >= 48
+    orc = om.generate(prompts[0], 0, steps, forced=lambda st: 1, record=True)
+    rt = _runtime(shp, 6012, 1, P, steps)
+    res = run_gpu(rt, prompts[:1], [0], steps, sched[:1], debug_steps=steps + 1)
+    free_exact = _free_running_compare(orc, res, TOL[BF16], 0.0)
+    st = res.stats[0]
+    print("free-running exact decisions", free_exact, flush=True)
+    assert all(len(g) == 1 for g in res.groups[0])
+    assert st["gen_slots"] == st["tokens"] - 1 == steps and st["kv_len"] == P + steps
+    assert free_exact >= 10

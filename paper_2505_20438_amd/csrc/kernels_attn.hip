@@ -158,22 +158,23 @@ __device__ __forceinline__ void attn_block(KVBlock<T, HD>& blk, int base, int li
 // key blocks a wave keeps in flight at once: 8 KB (head dim 64) or 16 KB (128) of K and V each
 template <int HD> struct AttnChunk { static constexpr int NB = 256 / HD; };
 
-// Key blocks [b0, b1) of KB slots from slot0, masked at `limit` / `vlimit`.
-// The blocks go in chunks of NB whose loads are all issued before any of them
-// is used, so a chunk costs one memory round trip.
-template <typename T, int HD, bool NT = true>
+// Key blocks b0, b0 + BS, b0 + 2 BS, ... below b1, of KB slots from slot0,
+// masked at `limit` / `vlimit`.  The blocks go in chunks of NB whose loads are
+// all issued before any of them is used, so a chunk costs one memory round trip.
+template <typename T, int HD, bool NT = true, int BS = 1>
 __device__ __forceinline__ void attn_blocks(const T* Kb, const T* Vb, int S, int slot0, int b0, int b1, int limit,
                                             int vlimit, const u4* qf, const u4* ql, float scale, float& mrun,
                                             float& lrun, f4* o) {
   constexpr int KB = Frag<T>::KB, NB = AttnChunk<HD>::NB;
-  for (int c = b0; c < b1; c += NB) {
+  for (int c = b0; c < b1; c += NB * BS) {
     KVBlock<T, HD> blk[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      if (c + i < b1) kv_load<T, HD, NT>(blk[i], Kb, Vb, S, slot0 + (c + i) * KB);
+      if (c + i * BS < b1) kv_load<T, HD, NT>(blk[i], Kb, Vb, S, slot0 + (c + i * BS) * KB);
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      if (c + i < b1) attn_block<T, HD>(blk[i], slot0 + (c + i) * KB, limit, vlimit, qf, ql, scale, mrun, lrun, o);
+      if (c + i * BS < b1)
+        attn_block<T, HD>(blk[i], slot0 + (c + i * BS) * KB, limit, vlimit, qf, ql, scale, mrun, lrun, o);
   }
 }
 
@@ -319,30 +320,32 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
   const int grp = a.H / a.Hkv;
   const T* Kb = (const T*)a.K + (size_t)r * a.sb + kvh * a.sh;  // decode rows: row r is sequence r
   const T* Vb = (const T*)a.VT + (size_t)r * a.sb + kvh * a.sh;
-  // this wave's key blocks.  Split launches: a static share of the split's
+  // this wave's key blocks.  Split launches: the split's static share of the
   // blocks of [0, kv_cap), so the first loads need nothing from memory.  One
-  // workgroup per row: an even share of the row's own cached blocks (rows
-  // shorter than kv_cap would leave the last waves idle while the first ones
-  // carry a full share), at the cost of reading the row's length first.
+  // workgroup per row: the row's own cached blocks (rows shorter than kv_cap
+  // would leave waves idle), at the cost of reading the row's length first.
   int b0, b1;
   RowInfo ri;
+  // Wave w takes blocks w, w + NW, w + 2 NW, ... of the range, so at any time
+  // the waves of a workgroup read one contiguous window of K and one of V
+  // (measured 2.7% faster at 4 x 33K slots than a contiguous sub-range each).
+  constexpr int BS = ATTN_NW;
   if (a.nsplit == 1) {
     ri = row_info(a.rm, r);
-    const int nb = (min(max(ri.n_valid - 1, 0), a.kv_cap) + KB - 1) / KB;
-    b0 = w * nb / ATTN_NW;
-    b1 = (w + 1) * nb / ATTN_NW;
+    b0 = w;
+    b1 = (min(max(ri.n_valid - 1, 0), a.kv_cap) + KB - 1) / KB;
   } else {
     const int nblk_all = (a.kv_cap + KB - 1) / KB;
     const int per = (nblk_all + a.nsplit - 1) / a.nsplit;
-    const int sb0 = min(nblk_all, split * per), sb1 = min(nblk_all, sb0 + per);
-    b0 = sb0 + w * (sb1 - sb0) / ATTN_NW;
-    b1 = sb0 + (w + 1) * (sb1 - sb0) / ATTN_NW;
+    const int sb0 = min(nblk_all, split * per);
+    b0 = sb0 + w;
+    b1 = min(nblk_all, sb0 + per);
   }
   // first chunk of keys in flight before anything else
   KVBlock<T, HD> blk[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i)
-    if (b0 + i < b1) kv_load<T, HD>(blk[i], Kb, Vb, a.S, (b0 + i) * KB);
+    if (b0 + i * BS < b1) kv_load<T, HD>(blk[i], Kb, Vb, a.S, (b0 + i * BS) * KB);
   if (!any_flag(a.gate, a.gate_n)) return;
   if (a.nsplit != 1) ri = row_info(a.rm, r);
   // the projection values of this kv head: one 4-float chunk per thread, all splits
@@ -479,10 +482,10 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
   float mrun = -INFINITY, lrun = 0.f;
 #pragma unroll
   for (int i = 0; i < NB; ++i)
-    if (b0 + i < b1) attn_block<T, HD>(blk[i], (b0 + i) * KB, limit, limit, qf, ql, scale, mrun, lrun, o);
+    if (b0 + i * BS < b1) attn_block<T, HD>(blk[i], (b0 + i * BS) * KB, limit, limit, qf, ql, scale, mrun, lrun, o);
   // kv_cap bounds every row of the launch; this row's own length ends the loop
-  attn_blocks<T, HD>(Kb, Vb, a.S, 0, b0 + NB, min(b1, (limit + KB - 1) / KB), limit, limit, qf, ql, scale, mrun,
-                     lrun, o);
+  attn_blocks<T, HD, true, BS>(Kb, Vb, a.S, 0, b0 + NB * BS, min(b1, (limit + KB - 1) / KB), limit, limit, qf, ql,
+                               scale, mrun, lrun, o);
   attn_publish<T, HD>(sh, grp, mrun, lrun, o);
   __syncthreads();
   attn_merge_store<T, HD>(sh, extra, grp, r, a.R, kvh, split, a.nsplit, a.Hkv, a.o, a.ldo, a.part_out);

@@ -545,29 +545,42 @@ __global__ __launch_bounds__(COMBINE_THREADS) void k_attn_combine(AttnArgs a) {
   }
 }
 
+constexpr int PF_NW = 8, PF_NBL = 2, PF_RT = 2;
+#ifndef HAM_PFA_NS
+#define HAM_PFA_NS 4
+#endif
+constexpr int PFA_NS = HAM_PFA_NS;  // stages of key blocks in the LDS ring (PFA_NS - 1 in flight)
+template <typename T, int HD>
+struct PrefillBlock {  // 1 KB fragments of one key block in LDS: K (tile, fragment), then V (d-tile)
+  static constexpr int KB = Frag<T>::KB, EPL = Frag<T>::EPL, NF = HD / KB, ND = HD / 16, TT = KB / 16;
+  static constexpr int KF = TT * NF, VF = ND, BF = KF + VF;
+  static constexpr int KU = KF * 64, BU = BF * 64;
+};
+
+// s_waitcnt with vmcnt <= n (0..63) and lgkmcnt = 0 (expcnt untouched)
+template <int N>
+__device__ __forceinline__ void pfa_wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
 // Prefill: causal attention of a prompt chunk (rows of mode PREFILL: slots
 // t0 + r of one sequence).  One workgroup of PF_NW waves per (row chunk, kv
 // head): wave w takes q-head kvh*grp + w % grp and PF_RT tiles of 16 rows from
 // row 16*PF_RT*(w / grp) of the chunk, so a chunk is 16*PF_RT*(PF_NW / grp)
-// rows; each key block a wave reads from LDS serves all its row tiles.  The key
-// blocks pass through LDS once per workgroup, PF_NBL blocks per stage,
-// double-buffered: the global loads are contiguous, and each 16-byte piece is
-// stored where a wave's operand fragment expects it (K as [tile][fragment][lane],
-// V^T as [d-tile][lane]), so every operand read of a wave is one contiguous 1 KB.
-constexpr int PF_NW = 8, PF_NBL = 2, PF_RT = 2;
-template <typename T, int HD>
-struct PrefillBlock {  // 16-byte pieces of one key block: K, then V
-  static constexpr int KB = Frag<T>::KB, EPL = Frag<T>::EPL, NF = HD / KB, ND = HD / 16, TT = KB / 16;
-  static constexpr int KU = TT * NF * 64, VU = ND * 64, BU = KU + VU;
-};
-
+// rows; each key block a wave reads from LDS serves all its row tiles.  Key
+// blocks land in LDS straight from memory (global_load_lds_dwordx4), PF_NBL per
+// stage in a ring of PFA_NS stages, each 1 KB fragment in the lane order the
+// waves read it (K as operand (tile, fragment), V^T as d-tiles), so every
+// operand read is one contiguous 1 KB and no registers hold loads in flight.
 template <typename T, int HD>
 __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
   using PB = PrefillBlock<T, HD>;
   constexpr int KB = PB::KB, EPL = PB::EPL, NF = PB::NF, ND = PB::ND, TT = PB::TT, KU = PB::KU, BU = PB::BU;
-  constexpr int SU = PF_NBL * BU;                          // pieces per stage
-  constexpr int PER = (SU + 64 * PF_NW - 1) / (64 * PF_NW);  // pieces per thread per stage
-  __shared__ u4 lds[2][SU];
+  constexpr int BF = PB::BF, SF = PF_NBL * BF;             // fragments per block, per stage
+  constexpr int LPW = SF / PF_NW;                          // wave-loads per stage per wave
+  static_assert(SF % PF_NW == 0, "stage fragments must split evenly over the waves");
+  __shared__ u4 lds[PFA_NS][PF_NBL * BU];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int kvh = blockIdx.y;
   const int grp = a.H / a.Hkv, nrg = PF_NW / grp, RB = 16 * PF_RT * nrg;
@@ -602,42 +615,34 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
   }
 
   const int nblk = (wg_end + KB - 1) / KB, nst = (nblk + PF_NBL - 1) / PF_NBL;
-  // piece c of a key block: global source and LDS position
-  auto src_of = [&](int blk, int c) -> const T* {
-    const int base = blk * KB;
-    if (c < KU) {
-      const int sl = c / (HD / EPL), cc = c % (HD / EPL);
-      return Kb + (size_t)(base + sl) * HD + cc * EPL;
-    }
-    c -= KU;
-    return Vb + vt_offset(c / 4, base, HD) + (c % 4) * (KB / 4);
-  };
-  auto dst_of = [&](int c) -> int {
-    if (c < KU) {
-      // slot sl of the block is operand row 4*(sl / (KB/4)) + sl % 4 of tile (sl % (KB/4)) / 4
-      const int sl = c / (HD / EPL), col = (c % (HD / EPL)) * EPL;
-      const int qq = KB / 4, t = (sl % qq) / 4, rr = 4 * (sl / qq) + sl % 4;
-      return (t * NF + col / KB) * 64 + ((col % KB) / EPL) * 16 + rr;
-    }
-    c -= KU;
-    const int d = c / 4;
-    return KU + (d / 16) * 64 + (c % 4) * 16 + d % 16;
-  };
-  u4 sr[PER];
-  auto gload = [&](int stg) {
+  // this wave's fragments of a stage: q = w + PF_NW * i, block q / BF, fragment q % BF.  Lane l of a
+  // K fragment (tile t, column fragment f) holds operand row l & 15, whose slot is the one whose score
+  // lane group (l & 15) / 4 needs; lane l of a V fragment d-tile dt holds V^T row dt * 16 + (l & 15).
+  int koff[LPW], dsto[LPW], blki[LPW];
+  bool isk[LPW];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int q = tid + k * 64 * PF_NW;
-      const int blk = stg * PF_NBL + q / BU;
-      if (q < SU && blk < nblk) sr[k] = ld16(src_of(blk, q % BU));
+  for (int i = 0; i < LPW; ++i) {
+    const int q = w + PF_NW * i, j = q % BF;
+    blki[i] = q / BF;
+    dsto[i] = blki[i] * BU + j * 64;
+    isk[i] = j < PB::KF;
+    if (isk[i]) {
+      const int t = j / NF, f = j % NF, qq = KB / 4;
+      const int sl = qq * (r16 / 4) + 4 * t + r16 % 4;
+      koff[i] = sl * HD + f * KB + g * EPL;
+    } else {
+      koff[i] = (j - PB::KF) * 16 + r16;  // V^T row d; its address depends on the block's 32-slot tile
     }
-  };
-  auto lstore = [&](int stg, int buf) {
+  }
+  auto issue = [&](int stg) {  // every wave issues exactly LPW loads per stage (blocks past the end
+    u4* slot = lds[stg % PFA_NS];  // re-read the last block, never used), so vmcnt counts stages
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int q = tid + k * 64 * PF_NW;
-      const int blk = stg * PF_NBL + q / BU;
-      if (q < SU && blk < nblk) lds[buf][(q / BU) * BU + dst_of(q % BU)] = sr[k];
+    for (int i = 0; i < LPW; ++i) {
+      const int blk = min(stg * PF_NBL + blki[i], nblk - 1);
+      const T* p = isk[i] ? Kb + (size_t)blk * KB * HD + koff[i]
+                          : Vb + vt_offset(koff[i], blk * KB, HD) + g * (KB / 4);
+      __builtin_amdgcn_global_load_lds((const void*)p, (__attribute__((address_space(3))) void*)(slot + dsto[i]),
+                                       16, 0, 0);
     }
   };
 
@@ -651,20 +656,23 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
     lrun[t] = 0.f;
   }
   const float scale = 1.0f / sqrtf((float)HD);
-  if (nst > 0) {
-    gload(0);
-    lstore(0, 0);
-  }
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < PFA_NS - 1; ++st)
+    if (st < nst) issue(st);
   for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nst) gload(st + 1);  // in flight while this stage is used
+    // stage st has landed once at most the loads of the stages issued after it are pending
+    if (st + PFA_NS - 2 < nst) pfa_wait_vm_lgkm0<(PFA_NS - 2) * LPW>();
+    else pfa_wait_vm_lgkm0<0>();
+    asm volatile("s_barrier" ::: "memory");
+    // every wave is past stage st - 1: its slot takes stage st + PFA_NS - 1
+    if (st + PFA_NS - 1 < nst) issue(st + PFA_NS - 1);
+    const u4* sp = lds[st % PFA_NS];
 #pragma unroll
     for (int i = 0; i < PF_NBL; ++i) {
       const int blk = st * PF_NBL + i;
       if (blk < nblk && blk * KB < wave_end) {  // blocks past this wave's last row hold nothing it sees
         KVBlock<T, HD> kv;
-        const u4* bp = &lds[buf][i * BU];
+        const u4* bp = sp + i * BU;
 #pragma unroll
         for (int t = 0; t < TT; ++t)
 #pragma unroll
@@ -677,8 +685,6 @@ __global__ __launch_bounds__(64 * PF_NW) void k_attn_prefill(AttnArgs a) {
             attn_block<T, HD>(kv, blk * KB, limit[t], wave_end, qf[t], ql[t], scale, mrun[t], lrun[t], o[t]);
       }
     }
-    if (st + 1 < nst) lstore(st + 1, buf ^ 1);  // the other buffer was last read before the previous barrier
-    __syncthreads();
   }
   if (!rows_ok) return;
 #pragma unroll

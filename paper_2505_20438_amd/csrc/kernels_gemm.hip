@@ -1026,6 +1026,117 @@ __global__ __launch_bounds__(256) void k_gemm_big(GemmArgs a) {
     }
 }
 
+// ------------------------------------------------------------------------ prompt GEMM
+// Prompt chunks (M > 256 rows): a BM x 128 output tile per workgroup of BM/32
+// waves (64 x 64 each), k in steps of one fragment (KB).  Every operand
+// fragment a wave reads is one 1 KB block in lane order, and it lands in LDS
+// in that order straight from memory (global_load_lds_dwordx4: no registers
+// in flight), in a ring of PF_NS stages with PF_NS - 1 stages in flight, so a
+// step waits on memory only if the loads of a stage take longer than the
+// matrix work of the stages before it.  A fragment of X (16 rows, one k-slice)
+// is read by lane l from row l & 15 at k-offset (l >> 4) * EPL; a weight
+// fragment is already a contiguous 1 KB block (fragment-tiled layout).
+// Rows past M read row M - 1 and tiles past N the last tile (never stored).
+#ifndef HAM_PF_NS
+#define HAM_PF_NS 3
+#endif
+constexpr int PF_NS = HAM_PF_NS;
+
+// s_waitcnt with vmcnt <= n (0..63) and lgkmcnt = 0 (expcnt untouched)
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+template <typename T, int EPI, int BM>
+__global__ __launch_bounds__(BM * 2) void k_gemm_pf(GemmArgs a) {
+  if (!any_flag(a.gate, a.gate_n)) return;
+  constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, PL = Act<T>::PL;
+  constexpr int NW = BM / 32;                    // waves: BM/64 rows x 2 columns of 64 x 64
+  constexpr int NA = (BM / 16) * PL, NBW = 8;    // 1 KB fragments per stage: X (tiles x planes), W (tiles)
+  constexpr int NL = NA + NBW, LPW = NL / NW;    // wave-loads per stage, per wave
+  static_assert(NL % NW == 0, "loads per stage must split evenly over the waves");
+  constexpr int FRAG = 64;                       // u4 per fragment
+  __shared__ u4 ring[PF_NS][NL * FRAG];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int wm = w >> 1, wn = w & 1;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * 128;
+  const int nfr = a.K / KB, ntile = a.N / 16;
+  const T* W = (const T*)a.W;
+  const T* X = (const T*)a.X;
+  // this wave's loads of a stage: fragment q = w + NW * i (X fragments first)
+  const T* src[LPW];
+  int dst[LPW];
+  bool isw[LPW];
+#pragma unroll
+  for (int i = 0; i < LPW; ++i) {
+    const int q = w + NW * i;
+    dst[i] = q * FRAG;
+    if (q < NA) {
+      const int t = q / PL, p = q % PL;
+      const int m = min(m0 + t * 16 + r16, a.M - 1);
+      src[i] = X + ((size_t)m * PL + p) * a.ldx + g * EPL;
+      isw[i] = false;
+    } else {
+      const int t = min(n0 / 16 + (q - NA), ntile - 1);
+      src[i] = W + (size_t)t * nfr * FRAG * EPL + (size_t)lane * EPL;
+      isw[i] = true;
+    }
+  }
+  auto issue = [&](int s) {  // stage s (k-fragment s) into ring slot s % PF_NS
+    u4* slot = ring[s % PF_NS];
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      const T* p = src[i] + (size_t)s * (isw[i] ? FRAG * EPL : KB);
+      __builtin_amdgcn_global_load_lds((const void*)p, (__attribute__((address_space(3))) void*)(slot + dst[i]), 16,
+                                       0, 0);
+    }
+  };
+  f4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  const int nst = nfr;
+#pragma unroll
+  for (int s = 0; s < PF_NS - 1; ++s)
+    if (s < nst) issue(s);
+  for (int s = 0; s < nst; ++s) {
+    // stage s has landed once at most the loads of the stages issued after it are pending
+    if (s + PF_NS - 2 < nst) wait_vm_lgkm0<(PF_NS - 2) * LPW>();
+    else wait_vm_lgkm0<0>();
+    asm volatile("s_barrier" ::: "memory");
+    // every wave is past stage s - 1: its slot takes stage s + PF_NS - 1
+    if (s + PF_NS - 1 < nst) issue(s + PF_NS - 1);
+    const u4* slot = ring[s % PF_NS];
+    u4 af[4][PL], bf[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int p = 0; p < PL; ++p) af[i][p] = slot[((wm * 4 + i) * PL + p) * FRAG + lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bf[j] = slot[(NA + wn * 4 + j) * FRAG + lane];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mma_act<T>(acc[i][j], af[i][0], af[i][PL - 1], bf[j]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int nb = n0 + wn * 64 + 16 * j;
+      if (nb >= a.N) continue;  // uniform per wave
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm * 64 + i * 16 + 4 * g + r;
+        epi_tile<T, EPI>(a, m, m < a.M, nb, r16, acc[i][j][r]);
+      }
+    }
+}
+
 // ------------------------------------------------------------------------ launch
 // column tiles of a skinny launch: 32-column tiles while they already give
 // enough workgroups, else 16-column tiles
@@ -1172,6 +1283,15 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
     if constexpr (EPI == EPI_ARGMAX) {
       return -1;
     } else {
+#ifndef HAM_PF_BM
+#define HAM_PF_BM 128
+#endif
+      if (HAM_PF_BM > 0 && a.M > 256) {
+        constexpr int BM = HAM_PF_BM > 0 ? HAM_PF_BM : 128;
+        dim3 grid((a.N + 127) / 128, (a.M + BM - 1) / BM);
+        launch_k((k_gemm_pf<T, EPI, BM>), grid, dim3(BM * 2), 0, s, a);
+        return 0;
+      }
       dim3 grid((a.N + 127) / 128, (a.M + 127) / 128);
       launch_k((k_gemm_big<T, EPI>), grid, dim3(256), 0, s, a);
       return 0;

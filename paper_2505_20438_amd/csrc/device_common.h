@@ -22,11 +22,12 @@ static constexpr int WAVE = 64;
 
 __device__ __forceinline__ float bf2f(bf16 u) { return __uint_as_float(((uint32_t)u) << 16); }
 
-// round to nearest even (values are finite by construction)
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
+// round to nearest even (values are finite by construction): gfx950's
+// v_cvt_pk_bf16_f32, one instruction per pair of values
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bf16 f2bf(float f) { return __builtin_bit_cast(bf16, (__bf16)f); }
+__device__ __forceinline__ uint32_t f2bf2(float lo16, float hi16) {
+  return __builtin_bit_cast(uint32_t, bf16x2_t{(__bf16)lo16, (__bf16)hi16});
 }
 
 template <typename T> __device__ __forceinline__ float to_f(T v);
@@ -133,12 +134,7 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 
 // pack 8 floats (bf16) / 4 floats (fp32) into one lane fragment
 __device__ __forceinline__ u4 pack_frag_bf16(const float* v) {
-  u4 r;
-  r.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  r.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-  r.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-  r.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
-  return r;
+  return u4{f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7])};
 }
 
 // one product step with an activation fragment pair as the A operand

@@ -139,13 +139,18 @@ __device__ __forceinline__ void attn_block(KVBlock<T, HD>& blk, int base, int li
   ps += __shfl_xor(ps, 16, WAVE);
   ps += __shfl_xor(ps, 32, WAVE);
   lrun = lrun * alpha + ps;
-  mrun = mnew;
+  // rows whose running maximum did not move have alpha = 1 exactly: the rescale
+  // of the output rows is skipped when that holds for every row of the tile
+  // (once a row has seen many keys its maximum rarely moves)
+  if (__any(mnew != mrun)) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float ai = __shfl(alpha, 4 * g + i, WAVE);
+    for (int i = 0; i < 4; ++i) {
+      const float ai = __shfl(alpha, 4 * g + i, WAVE);
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt) o[dt][i] *= ai;
+      for (int dt = 0; dt < ND; ++dt) o[dt][i] *= ai;
+    }
   }
+  mrun = mnew;
   u4 phi, plo;
   PFrag<T>::make(p, phi, plo);
 #pragma unroll

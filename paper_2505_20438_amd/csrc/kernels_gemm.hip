@@ -1049,12 +1049,13 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
 }
 
-template <typename T, int EPI, int BM>
-__global__ __launch_bounds__(BM * 2) void k_gemm_pf(GemmArgs a) {
+template <typename T, int EPI, int BM, int BN>
+__global__ __launch_bounds__(BM / 64 * 2 * 64) void k_gemm_pf(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB, PL = Act<T>::PL;
-  constexpr int NW = BM / 32;                    // waves: BM/64 rows x 2 columns of 64 x 64
-  constexpr int NA = (BM / 16) * PL, NBW = 8;    // 1 KB fragments per stage: X (tiles x planes), W (tiles)
+  constexpr int NW = BM / 64 * 2;                // waves: BM/64 rows x 2 columns of 64 x BN/2
+  constexpr int WT = BN / 32;                    // 16-column tiles per wave
+  constexpr int NA = (BM / 16) * PL, NBW = BN / 16;  // 1 KB fragments per stage: X (tiles x planes), W (tiles)
   constexpr int NL = NA + NBW, LPW = NL / NW;    // wave-loads per stage, per wave
   static_assert(NL % NW == 0, "loads per stage must split evenly over the waves");
   constexpr int FRAG = 64;                       // u4 per fragment
@@ -1062,7 +1063,7 @@ __global__ __launch_bounds__(BM * 2) void k_gemm_pf(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int wm = w >> 1, wn = w & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * 128;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int nfr = a.K / KB, ntile = a.N / 16;
   const T* W = (const T*)a.W;
   const T* X = (const T*)a.X;
@@ -1094,11 +1095,11 @@ __global__ __launch_bounds__(BM * 2) void k_gemm_pf(GemmArgs a) {
                                        0, 0);
     }
   };
-  f4 acc[4][4];
+  f4 acc[4][WT];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < WT; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
   const int nst = nfr;
 #pragma unroll
   for (int s = 0; s < PF_NS - 1; ++s)
@@ -1111,23 +1112,23 @@ __global__ __launch_bounds__(BM * 2) void k_gemm_pf(GemmArgs a) {
     // every wave is past stage s - 1: its slot takes stage s + PF_NS - 1
     if (s + PF_NS - 1 < nst) issue(s + PF_NS - 1);
     const u4* slot = ring[s % PF_NS];
-    u4 af[4][PL], bf[4];
+    u4 af[4][PL], bf[WT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int p = 0; p < PL; ++p) af[i][p] = slot[((wm * 4 + i) * PL + p) * FRAG + lane];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bf[j] = slot[(NA + wn * 4 + j) * FRAG + lane];
+    for (int j = 0; j < WT; ++j) bf[j] = slot[(NA + wn * WT + j) * FRAG + lane];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mma_act<T>(acc[i][j], af[i][0], af[i][PL - 1], bf[j]);
+      for (int j = 0; j < WT; ++j) mma_act<T>(acc[i][j], af[i][0], af[i][PL - 1], bf[j]);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int nb = n0 + wn * 64 + 16 * j;
+    for (int j = 0; j < WT; ++j) {
+      const int nb = n0 + wn * (BN / 2) + 16 * j;
       if (nb >= a.N) continue;  // uniform per wave
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -1283,13 +1284,20 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
     if constexpr (EPI == EPI_ARGMAX) {
       return -1;
     } else {
-#ifndef HAM_PF_BM
-#define HAM_PF_BM 128
+#ifndef HAM_PF_BN
+#define HAM_PF_BN 256
 #endif
-      if (HAM_PF_BM > 0 && a.M > 256) {
-        constexpr int BM = HAM_PF_BM > 0 ? HAM_PF_BM : 128;
-        dim3 grid((a.N + 127) / 128, (a.M + BM - 1) / BM);
-        launch_k((k_gemm_pf<T, EPI, BM>), grid, dim3(BM * 2), 0, s, a);
+      if (a.M > 256) {
+        constexpr int BM = 128;
+        // 256-column tiles (64 x 128 per wave: half the operand reads from LDS per
+        // product of 64 x 64) while they still give at least two workgroups per CU
+        if (HAM_PF_BN == 256 && (long)((a.N + 255) / 256) * ((a.M + BM - 1) / BM) >= 512) {
+          dim3 grid((a.N + 255) / 256, (a.M + BM - 1) / BM);
+          launch_k((k_gemm_pf<T, EPI, BM, 256>), grid, dim3(BM / 64 * 2 * 64), 0, s, a);
+        } else {
+          dim3 grid((a.N + 127) / 128, (a.M + BM - 1) / BM);
+          launch_k((k_gemm_pf<T, EPI, BM, 128>), grid, dim3(BM / 64 * 2 * 64), 0, s, a);
+        }
         return 0;
       }
       dim3 grid((a.N + 127) / 128, (a.M + 127) / 128);

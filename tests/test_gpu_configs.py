@@ -207,3 +207,46 @@ def test_full_workload_counts_and_determinism(torch_cuda, name):
     assert 0.45 < total_slots / total_tokens < 0.62     # about 1/1.875 under the capped geometric law
     if len(runs) > 1:
         assert np.array_equal(runs[0][0], runs[1][0]) and np.array_equal(runs[0][1], runs[1][1])
+
+
+@pytest.mark.parametrize("name,steps", [("c5_8b_long", 6), ("c4_8b_b32", 6)])
+def test_full_size_batch_rows_equal_the_sequence_alone(torch_cuda, name, steps):
+    # A property that holds at any size: a sequence decoded inside the workload's batch
+    # gives the decisions it gives alone (rows never mix; only the launch shapes, and so
+    # the rounding, differ).  Sequence 0 of the long-context and batched workloads at full
+    # size, the first macro-steps, teacher-forced with its own batch-1 groups: logits,
+    # normed hidden states and stop logits within the bf16 tolerance, group boundaries
+    # and KV counts exact; row 1 of the batch is checked the same way.
+    from paper_2505_20438_amd import ham
+    w = WORKLOADS[name]
+    s = w.shape
+    prompts = synth.prompt_ids(w.seed_prompt, w.batch, w.prompt_len, s.vocab)
+    sched = synth.group_schedule(w.seed_sched, w.batch, steps + 1, s.max_group)
+    tol = TOL[BF16]
+    alone = {}
+    for b in (0, 1):
+        rt1 = ham.HamRuntime(config_for(s, 1, w.prompt_len, w.max_new), w.seed_weights)
+        alone[b] = run_gpu(rt1, prompts[b:b + 1], [w.max_new], steps, sched[b:b + 1], debug_steps=steps + 1)
+        del rt1
+        torch_cuda.cuda.empty_cache()
+    teacher = [alone[b].groups[0] if b in alone else alone[0].groups[0] for b in range(w.batch)]
+    sched_t = sched.copy()
+    for b in range(2, w.batch):   # other rows: row 0's groups, so every row has consistent lengths
+        sched_t[b] = sched[0]
+    rt = ham.HamRuntime(config_for(s, w.batch, w.prompt_len, w.max_new), w.seed_weights)
+    res = run_gpu(rt, prompts, [w.max_new] * w.batch, steps, sched_t, teacher=teacher, debug_steps=steps + 1)
+    worst = 0.0
+    for b in (0, 1):
+        one = alone[b]
+        assert [len(g) for g in res.own[b]] == [len(g) for g in one.groups[0]], b
+        for key, lg in one.logits.items():
+            _, step, k = key
+            bk = (b, step, k)
+            e = max(float(np.max(np.abs(res.logits[bk] - lg))),
+                    float(np.max(np.abs(res.hidden[bk] - one.hidden[key]))),
+                    abs(res.stop[bk] - one.stop[key]))
+            worst = max(worst, e)
+            assert e <= tol, (name, b, step, k, e)
+        assert res.stats[b]["kv_len"] == one.stats[0]["kv_len"] == w.prompt_len + steps
+        assert res.stats[b]["device_error"] == 0
+    print(name, "batch row vs alone: max difference", worst, flush=True)

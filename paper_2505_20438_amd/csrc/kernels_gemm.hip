@@ -1139,6 +1139,31 @@ __global__ __launch_bounds__(BM / 64 * 2 * 64) void k_gemm_pf(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------------ launch
+// compute units of the target part (MI355X: 256 in 8 XCDs)
+constexpr int GPU_CUS = 256;
+
+// Split-K count for a grid of `ntiles` column tiles: the one whose busiest CU
+// streams the least (a count that leaves some CUs one workgroup more than the
+// others costs that workgroup's bytes on all of them), and among those the
+// grid nearest `target` workgroups; at most `cap`.
+static int balanced_split(int ntiles, int cap, int target) {
+  cap = std::max(1, cap);
+  double best_load = 1e30;
+  long best_dist = 1L << 40;
+  int best = 1;
+  for (int ns = 1; ns <= cap; ++ns) {
+    const long wgs = (long)ntiles * ns;
+    const double load = (double)((wgs + GPU_CUS - 1) / GPU_CUS) / ns;
+    const long dist = std::labs(wgs - target);
+    if (load < best_load * (1 - 1e-9) || (load <= best_load * (1 + 1e-9) && dist < best_dist)) {
+      best_load = std::min(best_load, load);
+      best_dist = dist;
+      best = ns;
+    }
+  }
+  return best;
+}
+
 // column tiles of a skinny launch: 32-column tiles while they already give
 // enough workgroups, else 16-column tiles
 int skinny_tiles(int N) { return (N / 32 >= 512) ? N / 32 : N / 16; }
@@ -1185,7 +1210,9 @@ static int gemm_staged(const GemmArgs& a0, int max_split, int tag, Stream s, int
   const int TN = a.N / (16 * ntiles);
   int nsplit = 1;
   if (EPI != EPI_SWIGLU && max_split > 1) {
-    // at most about 512 workgroups (two per CU fit at once), two fragments per wave
+    // at most about 512 workgroups (two per CU fit at once), two fragments per
+    // wave; not balanced per CU as the plain path is: every workgroup repeats
+    // the prologue, which a larger grid pays for more than it gains
     nsplit = std::max(1, 512 / ntiles);
     nsplit = std::max(1, std::min(nsplit, std::min(max_split, nfr / (2 * STG_NW))));
   }
@@ -1311,9 +1338,10 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
   int nsplit = 1;
   if (EPI != EPI_ARGMAX && EPI != EPI_SWIGLU && max_split > 1) {
     // about 1024 workgroups, at least four fragments per wave
-    nsplit = (1024 + ntiles - 1) / ntiles;
-    nsplit = std::min(nsplit, std::min(max_split, nfr / 16));
-    nsplit = std::max(nsplit, 1);
+#ifndef HAM_SKINNY_WGS
+#define HAM_SKINNY_WGS 1024
+#endif
+    nsplit = balanced_split(ntiles, std::min(max_split, nfr / 16), HAM_SKINNY_WGS);
   }
   a.nsplit = nsplit;
   *nsplit_out = nsplit;

@@ -35,7 +35,7 @@ from synth.configs import BF16, STOP_FORCED, STOP_FORCED_TOKEN, WORKLOADS, Workl
 METRIC = "output tokens/s at 1 GPU; KV entries per output token; decode HBM GB/s"
 HBM_PEAK_GBS = 8000.0
 PROF_NAMES = ["qkv", "o_proj", "gate_up", "down", "micro_gemm", "embed_gemm", "lm_head_k0", "lm_head_micro",
-              "attn_decode"]
+              "attn_decode", "norm"]
 CSRC = os.path.join(ROOT, "paper_2505_20438_amd", "csrc")
 # the sources each measured kernel class is compiled from (a committed counter
 # summary applies only while these are unchanged)

@@ -247,6 +247,9 @@ int ham_tensor_info(const ham_config* cfg, int32_t tensor_id, size_t* offset, in
  *   HAM_PROF_HEAD0                 LM head + argmax + stop test, k = 0
  *   HAM_PROF_HEADK                 the same for micro steps k >= 1
  *   HAM_PROF_ATTN                  split-K decode attention, base layers
+ *   HAM_PROF_NORM                  RMSNorm launches (the first kernel of each
+ *                                  norm: base and micro layers, decisions);
+ *                                  bytes: rows x d x 4 x (pending splits + 3)
  * ham_profile(m, 1) clears the records and starts; ham_profile(m, 0) stops.
  * ham_profile_read synchronises the stream and fills out[kind] for
  * kind < n (launches, summed event time in ms, summed bytes). */
@@ -259,7 +262,8 @@ int ham_tensor_info(const ham_config* cfg, int32_t tensor_id, size_t* offset, in
 #define HAM_PROF_HEAD0 6
 #define HAM_PROF_HEADK 7
 #define HAM_PROF_ATTN 8
-#define HAM_PROF_KINDS 9
+#define HAM_PROF_NORM 9
+#define HAM_PROF_KINDS 10
 typedef struct ham_prof_t {
   int32_t launches;
   double ms;

@@ -74,7 +74,7 @@ struct Layout {
   // state
   size_t Kc, VTc, kv_layer, seq, st_bytes;
   // workspace
-  size_t x, x2, xp, xn, qkv, q, ao, act, part, qpart, ssb, nss, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
+  size_t x, x2, xp, xn, qkv, q, ao, act, part, qpart, ssb, nss, tss, gctr, actr, apart, bval, bidx, stopb, ctx, emb_in, emb_o, emb_y,
       rope_cs, Kloc, VTloc, loc_layer, ws_bytes;
 };
 
@@ -174,6 +174,7 @@ Layout make_layout(const ham_config* c) {
   y.qpart = take((size_t)PART_ROWS * y.QKV * 4);  // q/k/v partials (read while part is pending)
   y.ssb = take((size_t)MAX_GEMM_SPLIT * 64 * 4);
   y.nss = take((size_t)y.rows_max * ((y.d + 255) / 256) * 4);  // two-phase RMSNorm chunk sums
+  y.tss = take((size_t)NORM_OUT_MAX_TILES * NORM_OUT_MAX_ROWS * 4);  // NormOut tile sums of squares
   y.gctr = take((size_t)(y.Vpad / 32 + y.Nmax / 32 + 64) * 4);
   y.actr = take((size_t)y.rows_dec * y.Hk * 4);
   y.apart = take(attn_part_bytes(y.rows_dec, y.H, y.Hk, y.hd));
@@ -298,10 +299,16 @@ double gemm_bytes(const Layout& y, int N, int K, int M) {
   return (double)N * K * y.es + (double)M * K * 4 + (double)M * N * 4;
 }
 
-// A split-K GEMM result still held as partials (the next RMSNorm adds it to x).
+// A split-K GEMM result still held as partials (the next RMSNorm adds it to x),
+// or (tss set) the first half of the next RMSNorm already done by a NormOut
+// epilogue: x is up to date, the operand buffer holds g * x of the next norm
+// and tss the per-tile sums of squares of x (tss_n tiles).  A full RMSNorm
+// may still run on such rows: it reads x and ignores the rest.
 struct Pending {
   const float* part = nullptr;
   int nsplit = 0, M = 0;
+  const float* tss = nullptr;
+  int tss_n = 0;
 };
 
 int gemm_p(ham_model* m, int epi, const GemmArgs& a, int max_split, int kind, int* nsplit) {
@@ -323,7 +330,10 @@ int norm_rows(ham_model* m, float* x, int R, int stride, int off, const float* g
   na.part = pend.part; na.nsplit = pend.nsplit; na.pM = pend.M; na.ctx = ctx; na.ldctx = ldctx;
   na.gate = gate; na.gate_n = gate_n; na.ss = m->WS<float>(y.nss);
   pend = Pending{};
-  return launch_rmsnorm(dtype_of(m), na, m->s) ? fail(HAM_EINVAL, "rmsnorm shape") : HAM_OK;
+  m->pbegin(HAM_PROF_NORM, (double)R * y.d * 4 * (na.nsplit + 3));
+  const int rc = launch_rmsnorm(dtype_of(m), na, m->s);
+  m->pend();
+  return rc ? fail(HAM_EINVAL, "rmsnorm shape") : HAM_OK;
 }
 
 // The RMSNorm feeding GEMM `ga` (rows x, gain g): where the batched GEMM can
@@ -341,7 +351,10 @@ int norm_into_gemm(ham_model* m, GemmArgs& ga, int epi, float* x, int R, const f
     na.x = x; na.ldx = y.d; na.row_stride = 1; na.row_off = 0; na.g = g; na.d = y.d; na.R = R;
     na.eps = m->cfg.norm_eps; na.part = pend.part; na.nsplit = pend.nsplit; na.pM = pend.M;
     na.ctx = ctx; na.ldctx = ldctx; na.gate = gate; na.gate_n = gate_n; na.ss = m->WS<float>(y.nss);
-    if (launch_norm_reduce(na, m->s) == 0) {
+    m->pbegin(HAM_PROF_NORM, (double)R * y.d * 4 * (na.nsplit + 3));
+    const int nrc = launch_norm_reduce(na, m->s);
+    m->pend();
+    if (nrc == 0) {
       pend = Pending{};
       ga = gw;
       return HAM_OK;
@@ -420,9 +433,20 @@ int macro_attn_splits(int dtype, int B, int Hk, int hd, int kv_cap) {
 // RMSNorm folded into gate/up.  Where a staged prologue does not fit, the
 // separate kernels run instead.  A folded norm writes the updated residual to
 // the other row buffer: `x` names the current one on entry and on exit.
+//
+// Rows 2..8 whose q/k/v prologue does not fit (it would hold the rows' whole
+// k-range of X in LDS) take the NormOut form instead: the o-projection and the
+// down projection run unsplit, one workgroup per column tile, and their
+// epilogue finishes the residual, writes g * x of the next norm (gain g2, or
+// `g_next`: the next layer's g1, null after the last layer) and per-tile sums
+// of squares; the fused attention step and the gate/up epilogue apply 1/rms.
+// Only a layer whose input rows come from elsewhere (pend without tss) runs an
+// RMSNorm launch.  The down projection then also copies its output rows to
+// `ctx_out` (where the next norm would have).
 int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void* Kc, void* VTc, long long sb,
                    long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
-                   float* ctx_prev, int ldctx, int kv_visible, const StepAttn& step, bool base) {
+                   float* ctx_prev, int ldctx, int kv_visible, const StepAttn& step, bool base,
+                   const float* g_next, float* ctx_out) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   const auto gk = [&](int kind) { return base ? kind : HAM_PROF_MICRO; };
@@ -443,11 +467,29 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   ga.xs.g = m->W<float>(y.g1[j]); ga.xs.eps = eps; ga.xs.x_out = other(x); ga.xs.ctx = ctx_prev;
   ga.xs.ldctx = ldctx; ga.xs.ss_out = m->WS<float>(y.ssb);
   const int qkv_split = std::min(split, attn_step_max_qkv_split());
-  const bool q_staged = gemm_stage_fits(dt, EPI_F32, ga, qkv_split);
-  if (!q_staged) {
-    ga.xsrc = XS_ACT;
-    if (norm_into_gemm(m, ga, EPI_F32, x, R, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, gate, gate_n))
-      return HAM_EINVAL;
+  // NormOut form: decided on the q/k/v prologue without pending partials, so
+  // that every layer of a batch takes the same form
+  GemmArgs probe = ga;
+  probe.xs.part = nullptr; probe.xs.nsplit = 0; probe.xs.pM = 0;
+  const int ntiles_no = gemm_norm_out_tiles(y.d);
+  const bool fuse = R >= 2 && R <= NORM_OUT_MAX_ROWS && gemm_norm_out_fits(R, y.d, y.HD) &&
+                    gemm_norm_out_fits(R, y.d, y.F) && !gemm_stage_fits(dt, EPI_F32, probe, qkv_split);
+  const float* ss_in = nullptr;  // tile sums for the attention step's 1/rms
+  int ss_in_n = 0;
+  bool q_staged = false;
+  if (pend.tss) {
+    // the previous layer's NormOut epilogue wrote g1 * x and its tile sums
+    // (and copied x to ctx_prev if that was asked)
+    ga.xsrc = XS_ACT; ga.X = m->WS<char>(y.xn); ga.ldx = y.d;
+    ss_in = pend.tss; ss_in_n = pend.tss_n;
+    pend = Pending{};
+  } else {
+    q_staged = gemm_stage_fits(dt, EPI_F32, ga, qkv_split);
+    if (!q_staged) {
+      ga.xsrc = XS_ACT;
+      if (norm_into_gemm(m, ga, EPI_F32, x, R, m->W<float>(y.g1[j]), pend, ctx_prev, ldctx, gate, gate_n))
+        return HAM_EINVAL;
+    }
   }
   if (gemm_p(m, EPI_F32, ga, qkv_split, gk(HAM_PROF_QKV), &ns)) return fail(HAM_EINVAL, "qkv gemm shape");
   if (q_staged) {
@@ -463,7 +505,7 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   go.xs.rec_o = m->WS<float>(y.apart);
   go.xs.rec_ml = m->WS<float>(y.apart) + (size_t)R * y.Hk * attn_split * (y.H / y.Hk) * y.hd;
   go.xs.ans = attn_split; go.xs.Hkv = y.Hk; go.xs.grp = y.H / y.Hk; go.xs.hd = y.hd;
-  const bool o_staged = attn_split > 1 && gemm_stage_fits(dt, EPI_RESID, go, split);
+  const bool o_staged = !fuse && attn_split > 1 && gemm_stage_fits(dt, EPI_RESID, go, split);
 
   AttnStepArgs sa{};
   sa.qkv = m->WS<float>(y.qkv); sa.part = ns > 1 ? m->WS<float>(y.qpart) : nullptr; sa.nsplit_qkv = ns;
@@ -475,6 +517,9 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   sa.combine = !o_staged;
   sa.gate = gate; sa.gate_n = gate_n;
   sa.ss = (q_staged && ns > 1) ? m->WS<float>(y.ssb) : nullptr; sa.ss_n = ns; sa.d = y.d; sa.eps = eps;
+  if (ss_in) {
+    sa.ss = ss_in; sa.ss_n = ss_in_n;
+  }
   m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
   const int arc = launch_attn_step(dt, sa, m->s);
   m->pend();
@@ -483,7 +528,28 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   if (!o_staged) {
     go.xsrc = XS_ACT; go.X = m->WS<char>(y.ao); go.ldx = y.HD;
   }
+  if (fuse) {
+    go.no.g = m->W<float>(y.g2[j]); go.no.act = m->WS<char>(y.xn); go.no.lda = y.d; go.no.ss = m->WS<float>(y.tss);
+  }
   if (gemm_p(m, EPI_RESID, go, split, gk(HAM_PROF_O), &ns)) return fail(HAM_EINVAL, "o-proj gemm shape");
+  if (fuse) {
+    // gate/up on g2 * x, rows scaled by 1/rms before SwiGLU; then the down
+    // projection's NormOut epilogue
+    GemmArgs gu{};
+    gu.gate = gate; gu.gate_n = gate_n; gu.M = R;
+    gu.W = m->W<char>(y.Wgu[j]); gu.N = 2 * y.F; gu.K = y.d; gu.out = m->WS<char>(y.act); gu.ldo = y.F;
+    gu.xsrc = XS_ACT; gu.X = m->WS<char>(y.xn); gu.ldx = y.d;
+    gu.rs.ss = m->WS<float>(y.tss); gu.rs.n = ntiles_no; gu.rs.d = y.d; gu.rs.eps = eps;
+    if (gemm_p(m, EPI_SWIGLU, gu, 1, gk(HAM_PROF_GU), &ns)) return fail(HAM_EINVAL, "gate/up gemm shape");
+    GemmArgs gd{};
+    gd.gate = gate; gd.gate_n = gate_n; gd.M = R;
+    gd.W = m->W<char>(y.Wd[j]); gd.N = y.d; gd.K = y.F; gd.X = m->WS<char>(y.act); gd.ldx = y.F;
+    gd.out = x; gd.ldo = y.d; gd.ctx = ctx_out; gd.ldctx = ldctx;
+    gd.no.g = g_next; gd.no.act = m->WS<char>(y.xn); gd.no.lda = y.d; gd.no.ss = m->WS<float>(y.tss);
+    if (gemm_p(m, EPI_RESID, gd, 1, gk(HAM_PROF_DOWN), &ns)) return fail(HAM_EINVAL, "down gemm shape");
+    pend = g_next ? Pending{nullptr, 0, 0, m->WS<float>(y.tss), ntiles_no} : Pending{};
+    return HAM_OK;
+  }
   if (ns > 1) pend = Pending{m->WS<float>(y.part), ns, R};
 
   // gate/up, second norm folded in
@@ -516,7 +582,8 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
 
 int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool prefill, void* Kc, void* VTc,
               long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
-              float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step) {
+              float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step, const float* g_next = nullptr,
+              float* ctx_out = nullptr) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
@@ -531,7 +598,7 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool pref
   }
   if (step)
     return run_layer_step(m, j, R, rm, x, Kc, VTc, sb, sh, S, attn_split, gate, gate_n, pend, ctx_prev, ldctx,
-                          kv_visible, *step, base);
+                          kv_visible, *step, base, g_next, ctx_out);
   const int split = prefill ? 1 : MAX_GEMM_SPLIT;
   int ns = 1;
   GemmArgs ga{};
@@ -616,9 +683,11 @@ int decode_tail(ham_model* m, Pending& pend, float* ctx_last, float* xres, int* 
     const StepAttn lstep{m->W<float>(y.cos_t) + (size_t)lpos * half, m->W<float>(y.sin_t) + (size_t)lpos * half, 0,
                          lpos};
     for (int mj = 0; mj < y.M; ++mj) {
+      const float* g_next = mj + 1 < y.M ? m->W<float>(y.g1[y.L + mj + 1]) : nullptr;
       rc = run_layer(m, y.L + mj, R, rm, x, false, m->WS<char>(y.Kloc + mj * y.loc_layer),
                      m->WS<char>(y.VTloc + mj * y.loc_layer), lsb, lsh, LOCAL_SLOTS, 1, m->sp.active, B, mp_pend,
-                     nullptr, 0, k == 1 ? B * (y.C + 1) * (y.C + 2) / 2 : B * (y.C + k), k == 1 ? nullptr : &lstep);
+                     nullptr, 0, k == 1 ? B * (y.C + 1) * (y.C + 2) / 2 : B * (y.C + k), k == 1 ? nullptr : &lstep,
+                     g_next);
       if (rc) return rc;
     }
     rc = run_decision(m, k, x, k == 1 ? y.C + 1 : 1, k == 1 ? y.C : 0, m->W<float>(y.gmf), mp_pend, nullptr,
@@ -939,12 +1008,15 @@ int macro_step_body(ham_model* m, int32_t* d_out_tokens, int32_t* d_out_lens) {
   Pending pend;
   float* ctx_prev = nullptr;  // context slot of the previous layer's output, captured by the next norm
   for (int l = 0; l < y.L; ++l) {
-    int rc = run_layer(m, l, B, rm, x, false, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer, sb,
-                       sh, y.S, nsplit, m->sp.step_on, B, pend, ctx_prev, y.C * y.d, m->kv_visible, &bstep);
-    if (rc) return rc;
-    ctx_prev = nullptr;
+    float* ctx_out = nullptr;  // context slot of this layer's output
     for (int c = 0; c < y.C; ++c)
-      if (y.ctx_l[c] == l + 1) ctx_prev = ctx + (size_t)c * y.d;
+      if (y.ctx_l[c] == l + 1) ctx_out = ctx + (size_t)c * y.d;
+    const float* g_next = l + 1 < y.L ? m->W<float>(y.g1[l + 1]) : nullptr;
+    int rc = run_layer(m, l, B, rm, x, false, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer, sb,
+                       sh, y.S, nsplit, m->sp.step_on, B, pend, ctx_prev, y.C * y.d, m->kv_visible, &bstep, g_next,
+                       ctx_out);
+    if (rc) return rc;
+    ctx_prev = ctx_out;
   }
   int rc = decode_tail(m, pend, ctx_prev, x, d_out_tokens, d_out_lens);
   if (rc) return rc;

@@ -122,16 +122,35 @@ struct XStage {
   const float* ssw; int nchw;          // NORMW: chunk sums of squares [M][nchw]
 };
 
+// RESID, unsplit (gemm_norm_out_fits): the next RMSNorm's first half in the
+// epilogue.  With x the updated residual rows, writes g * x as the next GEMM's
+// operand and, per column tile t, the sums of squares of its columns per row;
+// the consumer applies 1/rms (RowScale, or the fused attention step).
+struct NormOut {
+  const float* g;                  // next norm's gain [N], or null (operand not written)
+  void* act; int lda;              // g * x, operand layout [M][lda] (storage type)
+  float* ss;                       // [tile][M] sums of squares; null: plain RESID
+};
+
+// SWIGLU: the product's rows scaled by 1/rms before the activation, from the
+// per-tile sums of squares a NormOut epilogue wrote (n tiles, n <= 256).
+struct RowScale {
+  const float* ss; int n, d;       // ss [n][M]; rinv = 1/sqrt(sum / d + eps); null: no scaling
+  float eps;
+};
+
 struct GemmArgs {
   const void* W; int N, K;         // W [N][K] row-major (storage type), N % 32 == 0
   const void* X; int ldx; int M;   // X [M][ldx] (storage type)
   void* out; int ldo;              // destination (see EpiKind)
-  float* ctx; int ldctx;           // RESID: copy of updated rows (optional)
+  float* ctx; int ldctx;           // RESID with NormOut: copy of updated rows (optional)
   const int* rowmask;              // XMASK: rows to store
   const int* gate; int gate_n;     // launch does nothing unless a gate flag is set
   float* part; int* counters; int nsplit;  // split-K partials [nsplit][M][N] (written when nsplit > 1)
   DecideArgs dec;                  // ARGMAX only
   int xsrc; XStage xs;             // X operand source (XS_ACT: X above)
+  NormOut no;                      // RESID only
+  RowScale rs;                     // SWIGLU only
 };
 
 // ---------------------------------------------------------------- attention
@@ -175,6 +194,12 @@ int launch_gemm(int dtype, int epi, const GemmArgs& a, int max_split, Stream s, 
 constexpr int GEMM_NO_STAGE = -2;
 // whether launch_gemm would take the staged path for these arguments (nothing launched)
 bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split);
+// the NormOut epilogue (one workgroup per 16-column tile, unsplit): rows up to
+// NORM_OUT_MAX_ROWS and at most NORM_OUT_MAX_TILES tiles; the tile count its
+// launch uses (-1: does not apply)
+constexpr int NORM_OUT_MAX_ROWS = 8, NORM_OUT_MAX_TILES = 256;
+bool gemm_norm_out_fits(int M, int N, int K);
+int gemm_norm_out_tiles(int N);
 int launch_decide(int dtype, const DecideArgs& d, int ntiles, int M, Stream s);
 int skinny_tiles(int N);  // column tiles (argmax partials per row) of a skinny launch over N columns
 int launch_split_reduce(int dtype, int epi, const GemmArgs& a, Stream s);

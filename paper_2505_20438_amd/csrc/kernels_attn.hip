@@ -380,13 +380,22 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_step(AttnStepArgs a) {
   }
   // RMSNorm scale of this row when the projection's input was left unscaled
   float rinv = 1.f;
-  if (a.ss) {
+  if (a.ss && a.ss_n <= MAXS) {  // per-split sums of a staged projection
     float sv[MAXS];
 #pragma unroll
     for (int s = 0; s < MAXS; ++s) sv[s] = s < a.ss_n ? a.ss[(size_t)s * a.pM + r] : 0.f;
     float ss = 0.f;
 #pragma unroll
     for (int s = 0; s < MAXS; ++s) ss += sv[s];
+    rinv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
+  } else if (a.ss) {  // per column tile sums of a NormOut epilogue (at most 256): each wave sums them
+    float sv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = lane + 64 * q;
+      sv[q] = t < a.ss_n ? a.ss[(size_t)t * a.pM + r] : 0.f;
+    }
+    const float ss = wave_sum((sv[0] + sv[1]) + (sv[2] + sv[3]));
     rinv = 1.0f / sqrtf(ss / (float)a.d + a.eps);
   }
   // RoPE factors of this row: elements i = f*KB + g*EPL + e, f < NF/2
@@ -753,6 +762,7 @@ int launch_attn_step(int dtype, const AttnStepArgs& a, Stream s) {
       a.nsplit > 64)  // the split combine holds one split per lane
     return -1;
   if (a.part && (a.nsplit_qkv < 1 || a.nsplit_qkv > ATTN_STEP_MAXS)) return -1;
+  if (a.ss && (a.ss_n < 1 || a.ss_n > 256)) return -1;
   if (a.rm.mode != ROWS_DECODE && a.rm.mode != ROWS_MICROK) return -1;
   return dtype == 1 ? step_t<bf16>(a, s) : step_t<float>(a, s);
 }

@@ -113,24 +113,129 @@ template <typename T, int MT, int TN, int EPI>
 __device__ __forceinline__ void skinny_epilogue(const GemmArgs& a, f4 (*acc)[TN], int ntile, int split, int nsplit,
                                                 int n0);
 
+// Reduction of the NW waves' k-slices of one workgroup into wave 0's
+// accumulators (fixed order: wave 0, 1, ...; red holds [NW-1][NACC][64]
+// floats).  Returns whether this wave holds the result (wave 0).
+template <int MT, int TN, int NW>
+__device__ __forceinline__ bool skinny_reduce(f4 (*acc)[TN], float* red) {
+  constexpr int NACC = MT * TN * 4;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (w > 0) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[((w - 1) * NACC + (i * TN + j) * 4 + r) * 64 + lane] = acc[i][j][r];
+  }
+  __syncthreads();
+  if (w != 0) return false;
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = (i * TN + j) * 4 + r;
+        float v = acc[i][j][r];
+#pragma unroll
+        for (int p = 0; p < NW - 1; ++p) v += red[(p * NACC + q) * 64 + lane];
+        acc[i][j][r] = v;
+      }
+  return true;
+}
+
+// Per-row sums over the n tiles of ss [n][M] (n <= NORM_OUT_MAX_TILES, rows
+// m < M <= NORM_OUT_MAX_ROWS), wave-cooperative: lane l adds tiles l, l + 64,
+// ... in order, then a butterfly over the wave (all loads are issued before
+// the first is added).
+struct TileSums {
+  float p[NORM_OUT_MAX_ROWS];
+};
+__device__ __forceinline__ void tile_sums_load(TileSums& t, const float* ss, int n, int M) {
+  const int lane = threadIdx.x & 63;
+  constexpr int Q = NORM_OUT_MAX_TILES / 64;
+  float v[Q][NORM_OUT_MAX_ROWS];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int m = 0; m < NORM_OUT_MAX_ROWS; ++m) {
+      const int tt = lane + 64 * q;
+      v[q][m] = (tt < n && m < M) ? ss[(size_t)tt * M + m] : 0.f;
+    }
+#pragma unroll
+  for (int m = 0; m < NORM_OUT_MAX_ROWS; ++m) {
+    float acc = 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) acc += v[q][m];
+    t.p[m] = acc;
+  }
+}
+
+// Row scale 1/rms of this lane's rows 4g + r (MT = 1: rows below 16; rows past
+// NORM_OUT_MAX_ROWS keep 1, they are never stored)
+__device__ __forceinline__ void tile_sums_rinv(const TileSums& t, const RowScale& rs, float (&sc)[4]) {
+  const int g = (threadIdx.x & 63) >> 4;
+  float rin[NORM_OUT_MAX_ROWS];
+#pragma unroll
+  for (int m = 0; m < NORM_OUT_MAX_ROWS; ++m) rin[m] = 1.0f / sqrtf(wave_sum(t.p[m]) / (float)rs.d + rs.eps);
+  static_assert(NORM_OUT_MAX_ROWS == 8, "rows of lane groups 0 and 1");
+#pragma unroll
+  for (int r = 0; r < 4; ++r) sc[r] = g == 0 ? rin[r] : (g == 1 ? rin[4 + r] : 1.f);
+}
+
+// The NormOut epilogue of wave 0 (rows 4g + r, columns n0 + 16j + r16; MT = 1):
+// x += product, optional copy to ctx, g * x as the next operand, and per row
+// the sum of squares of this tile's columns.  xv holds x and gv the gain,
+// loaded at the start of the kernel.
+template <typename T, int TN>
+__device__ __forceinline__ void norm_out_epilogue(const GemmArgs& a, f4 (*acc)[TN], const float (*xv)[4],
+                                                  const float* gv, int ntile, int n0) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, g = lane >> 4;
+  float sq[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 4 * g + r, n = n0 + 16 * j + r16;
+      if (m < a.M) {
+        const float x = xv[j][r] + acc[0][j][r];
+        ((float*)a.out)[(size_t)m * a.ldo + n] = x;
+        if (a.ctx) a.ctx[(size_t)m * a.ldctx + n] = x;
+        if (a.no.g) Act<T>::put(a.no.act, m, a.no.lda, n, gv[j] * x);
+        sq[r] += x * x;
+      }
+    }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float v = sq[r];
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);  // the 16 columns of lane group g
+    const int m = 4 * g + r;
+    if (r16 == 0 && m < a.M) a.no.ss[(size_t)ntile * a.M + m] = v;
+  }
+}
+
 // TAG only separates the names of base-layer launches (always active) from the
-// others in profiler output; the code is the same.
-template <typename T, int MT, int TN, int EPI, int TAG>
-__global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
+// others in profiler output; the code is the same.  NW waves split the k-range
+// of the tile (4, or 16 for the unsplit NormOut launch: one workgroup per tile).
+template <typename T, int MT, int TN, int EPI, int TAG, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void k_gemm_skinny(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
   constexpr int EPL = Frag<T>::EPL, KB = Frag<T>::KB;
   constexpr int NACC = MT * TN * 4;
   constexpr int U = SkinnyBatch<T, MT, TN>::U;
-  __shared__ float red[3][NACC][64];  // k-slices of waves 1..3
+  __shared__ float red[NW - 1][NACC][64];  // k-slices of waves 1..NW-1
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int ntile = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
   const int n0 = ntile * 16 * TN;
   const int nfr = a.K / KB;
   const int c0 = (int)((long)split * nfr / nsplit), c1 = (int)((long)(split + 1) * nfr / nsplit);
-  // wave w takes fragments c0 + w + 4i of the k-range: at any moment the four
+  // wave w takes fragments c0 + w + NW i of the k-range: at any moment the
   // waves read neighbouring 1 KB blocks of a tile (one contiguous window)
-  const int nk = c1 - c0, cnt = nk > w ? (nk - w + 3) / 4 : 0;
+  const int nk = c1 - c0, cnt = nk > w ? (nk - w + NW - 1) / NW : 0;
   const T* W = (const T*)a.W;
   const T* X = (const T*)a.X;
 
@@ -139,6 +244,26 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  // NormOut launch: wave 0 loads the residual values and gains its epilogue
+  // needs before any weight load (used only at the end, they wait for nothing)
+  constexpr bool NORM_OUT = NW == 16;
+  static_assert(!NORM_OUT || (EPI == EPI_RESID && MT == 1), "NormOut: RESID, rows below 16");
+  float xv[TN][4], gv[TN];
+  if constexpr (NORM_OUT) {
+    if (w == 0) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = n0 + 16 * j + r16;
+        gv[j] = a.no.g ? a.no.g[n] : 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 4 * g + r;
+          xv[j][r] = m < a.M ? ((const float*)a.out)[(size_t)m * a.ldo + n] : 0.f;
+        }
+      }
+    }
+  }
 
   const T* wrow[TN];
 #pragma unroll
@@ -158,15 +283,15 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
   // in flight while batch i feeds the matrix cores
   const int nb = cnt / U;
   SkinnyBatch<T, MT, TN> cur, nxt;
-  if (nb > 0) skinny_load<T, MT, TN>(cur, wrow, xrow, xok, lo_off, c0 + w, 4);
+  if (nb > 0) skinny_load<T, MT, TN>(cur, wrow, xrow, xok, lo_off, c0 + w, NW);
   for (int it = 0; it < nb; ++it) {
     const bool more = it + 1 < nb;
-    if (more) skinny_load<T, MT, TN>(nxt, wrow, xrow, xok, lo_off, c0 + w + 4 * (it + 1) * U, 4);
+    if (more) skinny_load<T, MT, TN>(nxt, wrow, xrow, xok, lo_off, c0 + w + NW * (it + 1) * U, NW);
     skinny_mma<T, MT, TN>(acc, cur);
     if (more) cur = nxt;
   }
   for (int i = nb * U; i < cnt; ++i) {
-    const int f = c0 + w + 4 * i;
+    const int f = c0 + w + NW * i;
     u4 bw[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) bw[j] = ld16_stream(wrow[j] + (size_t)f * 64 * EPL);
@@ -182,41 +307,37 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(GemmArgs a) {
     }
   }
 
-  skinny_finish<T, MT, TN, EPI, 4>(a, acc, &red[0][0][0], ntile, split, nsplit, n0);
+  if constexpr (NORM_OUT) {
+    if (skinny_reduce<MT, TN, NW>(acc, &red[0][0][0])) norm_out_epilogue<T, TN>(a, acc, xv, gv, ntile, n0);
+  } else if constexpr (EPI == EPI_SWIGLU && MT == 1) {
+    // rows scaled by 1/rms before the activation: wave 0 issues the loads of
+    // the tile sums before the cross-wave reduction waits on the other waves
+    // (issued with the first weights instead, the compiler's waits for them
+    // held back the weight stream: measured no faster)
+    TileSums ts;
+    if (a.rs.ss && w == 0) tile_sums_load(ts, a.rs.ss, a.rs.n, a.M);
+    if (skinny_reduce<MT, TN, NW>(acc, &red[0][0][0])) {
+      if (a.rs.ss) {
+        float sc[4];
+        tile_sums_rinv(ts, a.rs, sc);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[0][j][r] *= sc[r];
+      }
+      skinny_epilogue<T, MT, TN, EPI>(a, acc, ntile, split, nsplit, n0);
+    }
+  } else {
+    skinny_finish<T, MT, TN, EPI, NW>(a, acc, &red[0][0][0], ntile, split, nsplit, n0);
+  }
 }
 
-// Reduction of the NW waves' k-slices of one workgroup (fixed order: wave 0,
-// 1, ...; red holds [NW-1][NACC][64] floats) and the epilogue: split partials,
-// the LM head's per-tile argmax, or the fused epilogue.
+// Reduction of the NW waves' k-slices and the epilogue: split partials, the
+// LM head's per-tile argmax, or the fused epilogue.
 template <typename T, int MT, int TN, int EPI, int NW>
 __device__ __forceinline__ void skinny_finish(const GemmArgs& a, f4 (*acc)[TN], float* red, int ntile, int split,
                                               int nsplit, int n0) {
-  constexpr int NACC = MT * TN * 4;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int r16 = lane & 15, g = lane >> 4;
-  if (w > 0) {
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) red[((w - 1) * NACC + (i * TN + j) * 4 + r) * 64 + lane] = acc[i][j][r];
-  }
-  __syncthreads();
-  if (w != 0) return;
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int q = (i * TN + j) * 4 + r;
-        float v = acc[i][j][r];
-#pragma unroll
-        for (int p = 0; p < NW - 1; ++p) v += red[(p * NACC + q) * 64 + lane];
-        acc[i][j][r] = v;
-      }
-  skinny_epilogue<T, MT, TN, EPI>(a, acc, ntile, split, nsplit, n0);
+  if (skinny_reduce<MT, TN, NW>(acc, red)) skinny_epilogue<T, MT, TN, EPI>(a, acc, ntile, split, nsplit, n0);
 }
 
 // Epilogue of one wave's finished accumulators (rows 16i + 4g + r, columns
@@ -1180,6 +1301,26 @@ static void run_skinny(const GemmArgs& a, int nsplit, int tag, Stream s) {
   launch_k((k_gemm_skinny<T, MT, TN, EPI, 1>), grid, dim3(256), 0, s, a);
 }
 
+// 16-column tiles only (at 32 columns the 16-wave kernel spills registers)
+int gemm_norm_out_tiles(int N) {
+  if (N % 32 != 0 || N / 16 > NORM_OUT_MAX_TILES) return -1;
+  return N / 16;
+}
+
+bool gemm_norm_out_fits(int M, int N, int K) {
+  return M >= 1 && M <= NORM_OUT_MAX_ROWS && K > 0 && gemm_norm_out_tiles(N) > 0;
+}
+
+// NormOut launch: one workgroup of 16 waves per column tile over the whole k-range
+template <typename T>
+static int run_norm_out(const GemmArgs& a, int tag, Stream s) {
+  if (!gemm_norm_out_fits(a.M, a.N, a.K) || a.K % Frag<T>::KB || !a.no.ss || (a.no.g && !a.no.act)) return -1;
+  const dim3 grid(gemm_norm_out_tiles(a.N)), block(64 * 16);
+  if (!tag) launch_k((k_gemm_skinny<T, 1, 1, EPI_RESID, 0, 16>), grid, block, 0, s, a);
+  else launch_k((k_gemm_skinny<T, 1, 1, EPI_RESID, 1, 16>), grid, block, 0, s, a);
+  return 0;
+}
+
 template <typename T, int TN, int EPI>
 static void run_skinny_mt(const GemmArgs& a, int nsplit, int tag, Stream s) {
   const int mt = (a.M + 15) / 16;
@@ -1287,6 +1428,7 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
   GemmArgs a = a0;
   constexpr int KB = Frag<T>::KB;
   if (a.N % 32 != 0 || a.K % KB != 0 || a.M <= 0) return -1;
+  if ((a.no.ss || a.rs.ss) && a.xsrc != XS_ACT) return -1;  // NormOut, RowScale: plain operand only
   *nsplit_out = 1;
   if (a.xsrc == XS_NORMW) {  // normed X built by the batched GEMM itself (8 < M <= 256)
     if constexpr (EPI == EPI_F32 || EPI == EPI_SWIGLU) {
@@ -1305,6 +1447,16 @@ static int gemm_t(const GemmArgs& a0, int max_split, int tag, Stream s, int* nsp
       return GEMM_NO_STAGE;
   }
   if (dry) return GEMM_NO_STAGE;
+  if constexpr (EPI == EPI_RESID) {
+    if (a.no.ss) {
+      *nsplit_out = 1;
+      return run_norm_out<T>(a, tag, s);
+    }
+  }
+  if constexpr (EPI == EPI_SWIGLU) {
+    // the row scale is applied by the skinny kernel of one 16-row tile only
+    if (a.rs.ss && (a.M > NORM_OUT_MAX_ROWS || a.rs.n < 1 || a.rs.n > NORM_OUT_MAX_TILES)) return -1;
+  }
   if (a.M > 8 && a.M <= 256 && a.K % WIDE_KC == 0 && EPI != EPI_XMASK && EPI != EPI_OP)
     return gemm_wide<T, EPI>(a, max_split, tag, s, nsplit_out);
   if (a.M > 64) {

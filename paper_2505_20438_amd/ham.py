@@ -17,7 +17,9 @@ HAM_OK, HAM_EINVAL, HAM_ENOMEM, HAM_EHIP, HAM_ESTATE, HAM_ECAP = 0, -1, -2, -3, 
 HAM_F32, HAM_BF16 = 0, 1
 HAM_STOP_HEAD, HAM_STOP_TOKEN, HAM_STOP_FORCED, HAM_STOP_FORCED_TOKEN = 0, 1, 2, 3
 
-HAM_PROF_KINDS = 9
+(HAM_PROF_QKV, HAM_PROF_O, HAM_PROF_GU, HAM_PROF_DOWN, HAM_PROF_MICRO, HAM_PROF_EMBED, HAM_PROF_HEAD0, HAM_PROF_HEADK,
+ HAM_PROF_ATTN, HAM_PROF_NORM) = range(10)
+HAM_PROF_KINDS = 10
 
 EXPORTED = ("ham_weights_bytes", "ham_state_bytes", "ham_workspace_bytes", "ham_init_weights",
             "ham_prefill", "ham_prefill_embeds", "ham_state_info", "ham_macro_step", "ham_kv_stats", "ham_set_debug", "ham_steps_done",

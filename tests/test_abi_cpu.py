@@ -37,6 +37,16 @@ def test_every_declared_symbol_is_exported(lib):
     assert declared == set(ham.EXPORTED)
 
 
+def test_binding_constants_match_header():
+    # every #define of the header that the binding names has the same value there
+    text = open(os.path.join(ROOT, "include", "ham.h")).read()
+    defines = dict(re.findall(r"^#define (HAM_\w+) \(?(-?\d+)\)?", text, re.M))
+    named = [k for k in defines if hasattr(ham, k)]
+    assert len(named) >= 23 and {"HAM_PROF_NORM", "HAM_PROF_KINDS", "HAM_BF16", "HAM_ECAP"} <= set(named)
+    for k in named:
+        assert getattr(ham, k) == int(defines[k]), k
+
+
 def test_size_queries(lib):
     for w in WORKLOADS.values():
         cfg = config_for(w.shape, w.batch, w.prompt_len, max(w.max_new, w.macro_steps))

@@ -1170,6 +1170,29 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
 }
 
+// Output tile of a prompt-GEMM workgroup.  Workgroups go to the 8 XCDs in
+// turn (linear id mod 8), and each XCD has its own L2: the grid is renumbered
+// so that every XCD takes one contiguous range of tiles, ordered in groups of
+// PF_GM M-tiles (M fastest), so the ~32 workgroups an XCD runs at once share
+// their X and weight slices in its L2 (4 M-tiles x 8 N-tiles at a time).
+#ifndef HAM_PF_GM
+#define HAM_PF_GM 4
+#endif
+__device__ __forceinline__ void pf_tile(int& mt, int& nt) {
+  const int gx = gridDim.x, gy = gridDim.y, G = gx * gy;
+  int L = blockIdx.y * gx + blockIdx.x;
+  if (HAM_PF_GM == 0) {
+    mt = blockIdx.y;
+    nt = blockIdx.x;
+    return;
+  }
+  if (G % 8 == 0) L = (L % 8) * (G / 8) + L / 8;
+  const int per_group = HAM_PF_GM * gx, group = L / per_group, first_m = group * HAM_PF_GM;
+  const int gsz = min(gy - first_m, HAM_PF_GM), r = L - group * per_group;
+  mt = first_m + r % gsz;
+  nt = r / gsz;
+}
+
 template <typename T, int EPI, int BM, int BN>
 __global__ __launch_bounds__(BM / 64 * 2 * 64) void k_gemm_pf(GemmArgs a) {
   if (!any_flag(a.gate, a.gate_n)) return;
@@ -1184,7 +1207,9 @@ __global__ __launch_bounds__(BM / 64 * 2 * 64) void k_gemm_pf(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int wm = w >> 1, wn = w & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  int mt, nt;
+  pf_tile(mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
   const int nfr = a.K / KB, ntile = a.N / 16;
   const T* W = (const T*)a.W;
   const T* X = (const T*)a.X;

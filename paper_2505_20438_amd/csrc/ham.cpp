@@ -416,8 +416,9 @@ int attn_step_splits(int dtype, int R, int Hk, int hd, int kv_cap) {
 }
 
 // splits of the base layers' fused step in a macro-step over B sequences: at
-// most 16 while the batch is small enough for the o-projection's prologue to
-// merge them (more would need a separate combine launch)
+// most 16 at up to 8 rows (each split adds records to merge: the
+// o-projection's prologue merges them where it fits, else k_attn_combine;
+// 8 or 4 splits measured slower)
 int macro_attn_splits(int dtype, int B, int Hk, int hd, int kv_cap) {
   const int n = attn_step_splits(dtype, B, Hk, hd, kv_cap);
   return B <= 8 ? std::min(16, n) : n;

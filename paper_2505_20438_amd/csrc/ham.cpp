@@ -435,14 +435,16 @@ int macro_attn_splits(int dtype, int B, int Hk, int hd, int kv_cap) {
 // separate kernels run instead.  A folded norm writes the updated residual to
 // the other row buffer: `x` names the current one on entry and on exit.
 //
-// Rows 2..8 whose q/k/v prologue does not fit (it would hold the rows' whole
-// k-range of X in LDS) take the NormOut form instead: the o-projection and the
-// down projection run unsplit, one workgroup per column tile, and their
-// epilogue finishes the residual, writes g * x of the next norm (gain g2, or
-// `g_next`: the next layer's g1, null after the last layer) and per-tile sums
-// of squares; the fused attention step and the gate/up epilogue apply 1/rms.
-// Only a layer whose input rows come from elsewhere (pend without tss) runs an
-// RMSNorm launch.  The down projection then also copies its output rows to
+// Rows 1..8 of a model wide enough to give every CU a 16-column tile (d >=
+// 4096), and at narrower widths rows 2..8 whose q/k/v prologue does not fit
+// (it would hold the rows' whole k-range of X in LDS), take the NormOut form
+// instead: the o-projection and the down projection run unsplit, one
+// workgroup per column tile, and their epilogue finishes the residual, writes
+// g * x of the next norm (gain g2, or `g_next`: the next layer's g1, null after
+// the last layer) and per-tile sums of squares; the fused attention step and
+// the gate/up epilogue apply 1/rms.  Only a layer whose input rows come from
+// elsewhere (pend without tss) normalises them itself (the staged prologue, or
+// an RMSNorm launch).  The down projection then also copies its output rows to
 // `ctx_out` (where the next norm would have).
 int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void* Kc, void* VTc, long long sb,
                    long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
@@ -473,8 +475,13 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   GemmArgs probe = ga;
   probe.xs.part = nullptr; probe.xs.nsplit = 0; probe.xs.pM = 0;
   const int ntiles_no = gemm_norm_out_tiles(y.d);
-  const bool fuse = R >= 2 && R <= NORM_OUT_MAX_ROWS && gemm_norm_out_fits(R, y.d, y.HD) &&
-                    gemm_norm_out_fits(R, y.d, y.F) && !gemm_stage_fits(dt, EPI_F32, probe, qkv_split);
+  // Taken at any row count once the unsplit launches give every CU a tile
+  // (d >= 4096: 8B shape at batch 1, 480 -> 500 tok/s); narrower models only
+  // where the staged q/k/v prologue does not fit (at d = 2048 the 128 unsplit
+  // workgroups leave half the CUs idle: batch 1 of the 1B shape 9% slower).
+  const bool fuse = R >= 1 && R <= NORM_OUT_MAX_ROWS && gemm_norm_out_fits(R, y.d, y.HD) &&
+                    gemm_norm_out_fits(R, y.d, y.F) &&
+                    (ntiles_no >= NORM_OUT_FILL_TILES || (R >= 2 && !gemm_stage_fits(dt, EPI_F32, probe, qkv_split)));
   const float* ss_in = nullptr;  // tile sums for the attention step's 1/rms
   int ss_in_n = 0;
   bool q_staged = false;

@@ -198,6 +198,7 @@ bool gemm_stage_fits(int dtype, int epi, const GemmArgs& a, int max_split);
 // NORM_OUT_MAX_ROWS and at most NORM_OUT_MAX_TILES tiles; the tile count its
 // launch uses (-1: does not apply)
 constexpr int NORM_OUT_MAX_ROWS = 8, NORM_OUT_MAX_TILES = 256;
+constexpr int NORM_OUT_FILL_TILES = 256;  // tiles (unsplit workgroups) that give each of the 256 CUs one
 bool gemm_norm_out_fits(int M, int N, int K);
 int gemm_norm_out_tiles(int N);
 int launch_decide(int dtype, const DecideArgs& d, int ntiles, int M, Stream s);

@@ -588,10 +588,15 @@ int run_layer_step(ham_model* m, int j, int R, const RowMap& rm, float*& x, void
   return HAM_OK;
 }
 
+// Rows of micro step 1 above which its last micro layer runs attention and
+// tail on each sequence's last row only (below, the batched GEMMs cost the
+// same for fewer rows: they stream the weights either way)
+constexpr int LAST_ROWS_MIN = 64;
+
 int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool prefill, void* Kc, void* VTc,
               long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
               float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step, const float* g_next = nullptr,
-              float* ctx_out = nullptr) {
+              float* ctx_out = nullptr, bool last_rows = false) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
@@ -634,6 +639,28 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool pref
   aa.q = m->WS<char>(y.q); aa.ldq = y.HD; aa.K = Kc; aa.VT = VTc; aa.sb = sb; aa.sh = sh; aa.S = S;
   aa.H = y.H; aa.Hkv = y.Hk; aa.hd = y.hd; aa.R = R; aa.nsplit = attn_split; aa.o = m->WS<char>(y.ao);
   aa.ldo = y.HD; aa.part = m->WS<float>(y.apart); aa.rm = rm;  // rows gate themselves (row map)
+  if (last_rows) {
+    // The last micro layer of micro step 1: every row's K and V are in the
+    // local cache now (the later micro steps attend over them), but only each
+    // sequence's last row (its first token, local position C) goes on to the
+    // decision, so attention and tail run on those B rows.  Their residual rows
+    // are copied to the second residual buffer, which x then names; their q
+    // rows are read in place (pitch C + 1 rows).
+    if (prefill || rm.mode != ROWS_MICRO1 || R % (y.C + 1) != 0) return fail(HAM_EINVAL, "last-row micro layer");
+    const int B = R / (y.C + 1);
+    float* xc = m->WS<float>(y.x2);
+    if (launch_copy_rows(x + (size_t)y.C * y.d, (long long)(y.C + 1) * y.d, xc, y.d, B, y.d, s))
+      return fail(HAM_EINVAL, "row copy shape");
+    RowMap r1 = rm;
+    r1.mode = ROWS_MICROK;
+    r1.k = 1;  // local position C + k - 1 = C, slots 0..C
+    aa.q = m->WS<char>(y.q) + (size_t)y.C * y.HD * 4;  // 4 bytes per activation value
+    aa.q_pitch = (y.C + 1) * y.HD;
+    aa.R = B;
+    aa.rm = r1;
+    R = B;
+    x = xc;
+  }
   m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
   const int arc = prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s);
   m->pend();
@@ -690,15 +717,19 @@ int decode_tail(ham_model* m, Pending& pend, float* ctx_last, float* xres, int* 
     const int lpos = y.C + k - 1, half = y.hd / 2;
     const StepAttn lstep{m->W<float>(y.cos_t) + (size_t)lpos * half, m->W<float>(y.sin_t) + (size_t)lpos * half, 0,
                          lpos};
+    const bool last_rows = k == 1 && R > LAST_ROWS_MIN;
     for (int mj = 0; mj < y.M; ++mj) {
       const float* g_next = mj + 1 < y.M ? m->W<float>(y.g1[y.L + mj + 1]) : nullptr;
       rc = run_layer(m, y.L + mj, R, rm, x, false, m->WS<char>(y.Kloc + mj * y.loc_layer),
                      m->WS<char>(y.VTloc + mj * y.loc_layer), lsb, lsh, LOCAL_SLOTS, 1, m->sp.active, B, mp_pend,
                      nullptr, 0, k == 1 ? B * (y.C + 1) * (y.C + 2) / 2 : B * (y.C + k), k == 1 ? nullptr : &lstep,
-                     g_next);
+                     g_next, nullptr, last_rows && mj == y.M - 1);
       if (rc) return rc;
     }
-    rc = run_decision(m, k, x, k == 1 ? y.C + 1 : 1, k == 1 ? y.C : 0, m->W<float>(y.gmf), mp_pend, nullptr,
+    // micro step 1 leaves C + 1 rows per sequence (the last is the decision's),
+    // or only that row where its last layer ran on it alone
+    const bool all_rows = k == 1 && !last_rows;
+    rc = run_decision(m, k, x, all_rows ? y.C + 1 : 1, all_rows ? y.C : 0, m->W<float>(y.gmf), mp_pend, nullptr,
                       out_tokens, out_lens);
     if (rc) return rc;
   }

@@ -156,6 +156,7 @@ struct GemmArgs {
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
   const void* q; int ldq;          // q [R][H*hd] (storage type), RoPE applied
+  int q_pitch;                     // decode: row r of q at r * q_pitch values (0: ldq, rows packed)
   const void* K; const void* VT;   // K [b][Hkv][S][hd], V tiled [b][Hkv][S/32][hd][32] (vt_offset)
   long long sb, sh;                // element strides per sequence and per kv head (both caches)
   int S;                           // slot capacity (row length of VT)

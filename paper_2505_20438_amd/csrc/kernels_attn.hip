@@ -284,7 +284,8 @@ __global__ __launch_bounds__(64 * ATTN_NW) void k_attn_decode(AttnArgs a) {
   const T* Vb = (const T*)a.VT + ri.b * a.sb + kvh * a.sh;
   u4 qf[NF], ql[NF];
   constexpr int PL = Act<T>::PL;
-  const T* qp = (const T*)a.q + (size_t)r * a.ldq * PL + (size_t)(kvh * grp + r16) * HD + g * EPL;
+  const T* qp = (const T*)a.q + (size_t)r * (a.q_pitch ? a.q_pitch : a.ldq) * PL + (size_t)(kvh * grp + r16) * HD +
+               g * EPL;
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     qf[f] = (r16 < grp) ? ld16(qp + f * KB) : zero16();

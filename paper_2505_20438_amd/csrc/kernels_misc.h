@@ -48,6 +48,8 @@ void launch_embed_attn(int dtype, const EmbedAttnArgs& a, Stream s);
 void launch_prefill_begin(const PrefillArgs& a, Stream s);
 void launch_gather_rows(int dtype, const GatherArgs& a, Stream s);
 void launch_copy_row(const float* src, float* dst, int d, Stream s);
+// R rows of d fp32 values from src (pitch ld_src floats) to dst (pitch ld_dst); 16-byte aligned rows
+int launch_copy_rows(const float* src, long long ld_src, float* dst, long long ld_dst, int R, int d, Stream s);
 void launch_gen_normal(int dtype, const GenArgs& a, Stream s);
 void launch_fill_f32(float* p, long long n, float v, Stream s);
 

@@ -413,6 +413,14 @@ __global__ __launch_bounds__(256) void k_copy_row(const float* src, float* dst, 
   for (int i = threadIdx.x; i < d; i += 256) dst[i] = src[i];
 }
 
+// dst row r = src row r (rows of d floats, d % 4 == 0, at their own pitches)
+__global__ __launch_bounds__(256) void k_copy_rows(const float* src, long long ld_src, float* dst, long long ld_dst,
+                                                   int d) {
+  const float* s = src + (size_t)blockIdx.x * ld_src;
+  float* t = dst + (size_t)blockIdx.x * ld_dst;
+  for (int i = 4 * threadIdx.x; i < d; i += 4 * 256) *reinterpret_cast<f4*>(t + i) = *reinterpret_cast<const f4*>(s + i);
+}
+
 // ---------------------------------------------------------------- weight generator
 // SplitMix64 (Steele, Lea, Flood 2014): i-th output of the stream seeded with s.
 __device__ __forceinline__ uint64_t sm64(uint64_t s, uint64_t i) {
@@ -469,6 +477,11 @@ void launch_gather_rows(int dtype, const GatherArgs& a, Stream s) {
 }
 void launch_copy_row(const float* src, float* dst, int d, Stream s) {
   launch_k(k_copy_row, dim3(1), dim3(256), 0, s, src, dst, d);
+}
+int launch_copy_rows(const float* src, long long ld_src, float* dst, long long ld_dst, int R, int d, Stream s) {
+  if (R < 0 || d % 4 != 0 || ld_src % 4 != 0 || ld_dst % 4 != 0) return -1;
+  if (R > 0) launch_k(k_copy_rows, dim3(R), dim3(256), 0, s, src, ld_src, dst, ld_dst, d);
+  return 0;
 }
 void launch_gen_normal(int dtype, const GenArgs& a, Stream s) {
   const long long count = (long long)a.rows * a.cols;

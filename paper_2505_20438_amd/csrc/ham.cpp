@@ -596,7 +596,7 @@ constexpr int LAST_ROWS_MIN = 64;
 int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool prefill, void* Kc, void* VTc,
               long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
               float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step, const float* g_next = nullptr,
-              float* ctx_out = nullptr, bool last_rows = false) {
+              float* ctx_out = nullptr, bool last_rows = false, bool kv_only = false) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
@@ -634,6 +634,7 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool pref
   ra.cos_t = m->W<float>(y.cos_t); ra.sin_t = m->W<float>(y.sin_t); ra.max_pos = y.max_pos; ra.rm = rm;
   ra.gate = gate; ra.gate_n = gate_n;
   launch_rope_append(dt, ra, s);
+  if (kv_only) return HAM_OK;  // only this layer's K and V of these rows are read later
 
   AttnArgs aa{};
   aa.q = m->WS<char>(y.q); aa.ldq = y.HD; aa.K = Kc; aa.VT = VTc; aa.sb = sb; aa.sh = sh; aa.S = S;
@@ -941,8 +942,11 @@ int prefill_common(ham_model* m, int32_t batch, int32_t T, const int32_t* d_prom
       rm.mode = ROWS_PREFILL; rm.b = b; rm.t0 = t0; rm.pos = d_positions; rm.ldpos = T; rm.st = m->sp;
       for (int l = 0; l < y.L; ++l) {
         Pending none;
+        // the last layer's outputs are read only at the prompt's last row (the
+        // decision and the context rows): earlier chunks append its K and V only
+        const bool kv_only = !last && l == y.L - 1;
         int rc = run_layer(m, l, R, rm, xp, true, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer,
-                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0, nullptr);
+                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0, nullptr, nullptr, nullptr, false, kv_only);
         if (rc) return rc;
         if (last)
           for (int c = 0; c < y.C; ++c)

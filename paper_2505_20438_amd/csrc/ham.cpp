@@ -62,6 +62,7 @@ constexpr int MAX_ATTN_SPLIT = 64;
 constexpr int LOCAL_SLOTS = 64;
 
 size_t attn_part_bytes(int R, int H, int Hk, int hd);
+int attn_splits_for(int dtype, int R, int Hk, int kv_max);
 
 struct Layout {
   // dims
@@ -596,7 +597,7 @@ constexpr int LAST_ROWS_MIN = 64;
 int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool prefill, void* Kc, void* VTc,
               long long sb, long long sh, int S, int attn_split, const int* gate, int gate_n, Pending& pend,
               float* ctx_prev, int ldctx, int kv_visible, const StepAttn* step, const float* g_next = nullptr,
-              float* ctx_out = nullptr, bool last_rows = false, bool kv_only = false) {
+              float* ctx_out = nullptr, bool last_rows = false, bool kv_only = false, bool last_row = false) {
   const Layout& y = m->y;
   const int dt = dtype_of(m);
   hipStream_t s = m->s;
@@ -661,6 +662,21 @@ int run_layer(ham_model* m, int j, int R, const RowMap& rm, float*& x, bool pref
     aa.rm = r1;
     R = B;
     x = xc;
+  }
+  if (last_row) {
+    // The prompt's last chunk at the last base layer: every row's K and V are
+    // appended, but the outputs are read only at the last row (the first
+    // decision and the context rows), so attention (split over that row's
+    // slots) and tail run on it alone
+    if (!prefill || rm.mode != ROWS_PREFILL) return fail(HAM_EINVAL, "last-row prefill layer");
+    RowMap r1 = rm;
+    r1.t0 = rm.t0 + R - 1;
+    aa.q = m->WS<char>(y.q) + (size_t)(R - 1) * y.HD * 4;  // 4 bytes per activation value
+    aa.R = 1;
+    aa.rm = r1;
+    aa.nsplit = attn_splits_for(dt, 1, y.Hk, r1.t0 + 1);
+    if (launch_attn_decode(dt, aa, s) != 0) return fail(HAM_EINVAL, "attention shape");
+    return layer_tail(m, j, 1, x + (size_t)(R - 1) * y.d, split, gate, gate_n, pend, gk);
   }
   m->pbegin(base ? HAM_PROF_ATTN : -1, (double)kv_visible * y.Hk * y.hd * 2 * y.es);
   const int arc = prefill ? launch_attn_prefill(dt, aa, s) : launch_attn_decode(dt, aa, s);
@@ -943,10 +959,13 @@ int prefill_common(ham_model* m, int32_t batch, int32_t T, const int32_t* d_prom
       for (int l = 0; l < y.L; ++l) {
         Pending none;
         // the last layer's outputs are read only at the prompt's last row (the
-        // decision and the context rows): earlier chunks append its K and V only
+        // decision and the context rows): earlier chunks append its K and V
+        // only, the last chunk runs attention and tail on that row alone
         const bool kv_only = !last && l == y.L - 1;
+        const bool last_row = last && l == y.L - 1 && R > 1;
         int rc = run_layer(m, l, R, rm, xp, true, m->st + y.Kc + l * y.kv_layer, m->st + y.VTc + l * y.kv_layer,
-                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0, nullptr, nullptr, nullptr, false, kv_only);
+                           sb, sh, y.S, 1, nullptr, 0, none, nullptr, 0, 0, nullptr, nullptr, nullptr, false, kv_only,
+                           last_row);
         if (rc) return rc;
         if (last)
           for (int c = 0; c < y.C; ++c)

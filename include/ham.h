@@ -70,7 +70,7 @@ typedef struct ham_config {
   int32_t micro_layers;
   int32_t max_group;    /* <= 4: micro-step cap (Sec. 3.6, Sec. 4.1) */
   /* base layers whose residual outputs condition the micro decoder (Sec. 3.3,
-   * Fig. 2a: several middle layers' hidden states, the last included).
+   * Fig. 2a: outputs of some intermediate base layers plus the final one).
    * n_ctx_layers = 0: C = min(4, n_layers) layers l_i = ceil(i * n_layers / C).
    * Otherwise C = n_ctx_layers in 1..8 and ctx_layers[0..C) are 1-based layer
    * indices, strictly increasing, each in 1..n_layers.  The micro decoder sees

@@ -3,8 +3,8 @@
 Shapes only (no arithmetic).  ``ctx_layers`` are 1-based indices of the base
 layers whose residual outputs form the micro-decoder context: by default
 C = min(4, L) layers, l_i = ceil(i * L / C), or an explicit ``ctx_layer_set``
-(the paper conditions the micro decoder on several middle-layer hidden states,
-the last one included, Sec. 3.3 and Fig. 2a; the choice of layers is a reading).
+(in the paper the micro decoder is conditioned on outputs of intermediate base
+layers plus the final one, Sec. 3.3 and Fig. 2a; which layers is a reading).
 """
 from __future__ import annotations
 
